@@ -1,0 +1,185 @@
+"""EFQ-Softmax CPU oracle -- test infrastructure only.
+
+Plain, slow implementations of what the GPU path computes, written from the
+paper (Alg. 1 inside Alg. 2, Secs. II-III).  The C file ``efq_oracle.c``
+holds the attention recurrence, P-gen and V quantiser; ``twin.py`` holds an
+independent numpy rendering of the P-gen and V-quant rules used to
+cross-check it.  Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU
+baseline of ``bench.py`` may import this package.  Nothing here imports the
+HIP package, and the HIP package never imports this.
+
+Parity pins that constrain these functions live in ``tests/test_oracle_*.py``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "efq_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+# Operating points (tau, h) of Sec. IV-A "Parameter selection".
+MEAN = (-3.06, 2.30)
+MMLU = (-2.90, 2.00)
+BALANCE = (-2.10, 2.70)
+# EFQ-Softmax-LUT constants of Sec. II-D: tau16 = log(1/24), h16 = 14/log 24.
+LUT = (float(np.log(1.0 / 24.0)), float(14.0 / np.log(24.0)))
+
+EFQ, EXPQ, EXACT, LUT_MODE = 0, 1, 2, 3
+
+C8 = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])  # Sec. II-B
+C16 = np.array([0, 1, 1, 1, 1, 1, 2, 2, 3, 3, 4, 5, 5, 6, 7, 7])  # Sec. II-D
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (no fast-math, no FMA contraction)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + f".tmp{os.getpid()}"
+        subprocess.run(
+            ["gcc", "-O2", "-std=gnu99", "-Wall", "-ffp-contract=off", "-fno-fast-math",
+             "-fopenmp", "-shared", "-fPIC", _SRC, "-o", tmp, "-lm"],
+            check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build(force=True)
+        L = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        L.orc_pgen.argtypes = [P, ctypes.c_long, ctypes.c_int, ctypes.c_int, ctypes.c_float,
+                               ctypes.c_float, P, P]
+        L.orc_pgen_real.argtypes = [P, ctypes.c_long, ctypes.c_int, ctypes.c_int,
+                                    ctypes.c_double, ctypes.c_double, P, P, P]
+        L.orc_quant_v.argtypes = [P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, P, P]
+        L.orc_attn.argtypes = [P, P, P] + [ctypes.c_int] * 6 + [
+            ctypes.c_float, ctypes.c_int, ctypes.c_int, ctypes.c_float, ctypes.c_float,
+            ctypes.c_int, P, ctypes.c_long, P, P, P, P, P, ctypes.c_int]
+        for f in (L.orc_pgen, L.orc_pgen_real, L.orc_quant_v, L.orc_attn):
+            f.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _params(mode: int, tau: Optional[float], h: Optional[float]):
+    if tau is None or h is None:
+        tau, h = LUT if mode == LUT_MODE else MEAN
+    return float(tau), float(h)
+
+
+def pgen(x: np.ndarray, mode: int = EFQ, tau: float = None, h: float = None):
+    """P-gen unit on shifted scores x (rows x cols fp32, -inf = masked).
+
+    Returns (codes uint8 [rows, cols], e8m0 uint8 [rows, ceil(cols/32)])."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if x.ndim == 1:
+        x = x[None, :]
+    rows, cols = x.shape
+    tau, h = _params(mode, tau, h)
+    codes = np.zeros((rows, cols), np.uint8)
+    e8 = np.zeros((rows, (cols + 31) // 32), np.uint8)
+    rc = lib().orc_pgen(_ptr(x), rows, cols, mode, tau, h, _ptr(codes), _ptr(e8))
+    assert rc == 0
+    return codes, e8
+
+
+def pgen_real(x: np.ndarray, lut: bool = False, tau: float = None, h: float = None):
+    """Alg. 1 evaluated step by step in fp64 (the real-valued reading).
+
+    Returns (codes, k_b int16, u = (z - tau) h in fp64)."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    if x.ndim == 1:
+        x = x[None, :]
+    rows, cols = x.shape
+    if tau is None or h is None:
+        tau, h = LUT if lut else MEAN
+    codes = np.zeros((rows, cols), np.uint8)
+    k = np.zeros((rows, (cols + 31) // 32), np.int16)
+    u = np.zeros((rows, cols), np.float64)
+    rc = lib().orc_pgen_real(_ptr(x), rows, cols, int(lut), float(tau), float(h), _ptr(codes),
+                             _ptr(k), _ptr(u))
+    assert rc == 0
+    return codes, k, u
+
+
+def quant_v(v_bits: np.ndarray):
+    """V [B, S, H, D] (bf16 bit patterns, uint16) -> MXFP4 along the key axis.
+
+    Returns (codes uint8 [B, H, nblk*32, D] with bit 3 = sign,
+             e8m0 uint8 [B, H, nblk, D])."""
+    v_bits = np.ascontiguousarray(v_bits, dtype=np.uint16)
+    B, S, H, D = v_bits.shape
+    nblk = (S + 31) // 32
+    codes = np.zeros((B, H, nblk * 32, D), np.uint8)
+    e8 = np.zeros((B, H, nblk, D), np.uint8)
+    rc = lib().orc_quant_v(_ptr(v_bits), B, S, H, D, _ptr(codes), _ptr(e8))
+    assert rc == 0
+    return codes, e8
+
+
+def all_rows(B: int, Hq: int, Sq: int) -> np.ndarray:
+    b, h, i = np.meshgrid(np.arange(B), np.arange(Hq), np.arange(Sq), indexing="ij")
+    return np.stack([b.ravel(), h.ravel(), i.ravel()], axis=1).astype(np.int32)
+
+
+def attn(q_bits, k_bits, v_bits, scale: float, causal: bool, mode: int = EFQ,
+         tau: float = None, h: float = None, bc: int = 64, rows: np.ndarray = None,
+         dump: bool = False, nthreads: int = 0):
+    """Attention forward for the listed query rows (Alg. 2 over tiles of bc keys).
+
+    q_bits [B, Sq, Hq, D], k_bits/v_bits [B, Sk, Hkv, D]: bf16 bit patterns.
+    rows: int32 [n, 3] of (b, hq, i); None = every row, ordered (b, hq, i).
+    Returns out [n, D] fp32, plus (codes [n, nblk*32], e8m0 [n, nblk],
+    m [n] fp32, l [n] fp64) when dump is set."""
+    q_bits = np.ascontiguousarray(q_bits, dtype=np.uint16)
+    k_bits = np.ascontiguousarray(k_bits, dtype=np.uint16)
+    v_bits = np.ascontiguousarray(v_bits, dtype=np.uint16)
+    B, Sq, Hq, D = q_bits.shape
+    _, Sk, Hkv, _ = k_bits.shape
+    if rows is None:
+        rows = all_rows(B, Hq, Sq)
+    rows = np.ascontiguousarray(rows, dtype=np.int32)
+    n = rows.shape[0]
+    tau, h = _params(mode, tau, h)
+    nblk = (Sk + 31) // 32
+    out = np.zeros((n, D), np.float32)
+    codes = e8 = mm = ll = None
+    if dump:
+        codes = np.zeros((n, nblk * 32), np.uint8)
+        e8 = np.zeros((n, nblk), np.uint8)
+        mm = np.zeros((n,), np.float32)
+        ll = np.zeros((n,), np.float64)
+    rc = lib().orc_attn(_ptr(q_bits), _ptr(k_bits), _ptr(v_bits), B, Sq, Sk, Hq, Hkv, D,
+                        float(scale), int(causal), int(mode), tau, h, int(bc), _ptr(rows), n,
+                        _ptr(out), _ptr(codes), _ptr(e8), _ptr(mm), _ptr(ll), int(nthreads))
+    if rc != 0:
+        raise ValueError(f"orc_attn failed with {rc}")
+    if dump:
+        return out, codes, e8, mm, ll
+    return out
+
+
+def bf16_bits(t) -> np.ndarray:
+    """Bit patterns of a bf16 torch tensor as a uint16 numpy array (a view of
+    the same values; no arithmetic)."""
+    import torch
+    return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+def bits_to_f64(b: np.ndarray) -> np.ndarray:
+    return (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
