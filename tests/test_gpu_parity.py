@@ -1,0 +1,215 @@
+"""GPU path vs the CPU oracle (run on an MI355X; every call goes through the C ABI).
+
+Bar: bit-exact E2M1 codes and E8M0 scales where the scores are bit-identical
+(the P-gen unit, and the fused kernel on exact-score inputs), attention
+output within 2e-3 max abs of the oracle's fp32 output.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_09721_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-3
+LN2 = math.log(2.0)
+
+
+@pytest.fixture(scope="module")
+def B():
+    from paper_2609_09721_amd import binding
+    binding.lib()
+    assert torch.cuda.is_available(), "no GPU"
+    return binding
+
+
+def adversarial_scores(rng, rows, cols, tau, h):
+    """Shifted scores with exact code thresholds, k-boundaries, masked keys,
+    denormals and very negative block maxima."""
+    x = -rng.exponential(2.5, size=(rows, cols)).astype(np.float32)
+    nblk = (cols + 31) // 32
+    for r in range(rows):
+        kind = r % 6
+        for b in range(nblk):
+            t0 = b * 32
+            n = min(32, cols - t0)
+            if kind == 0:       # block max 0 -> k = -3; neighbours of every threshold
+                x[r, t0] = 0.0
+                for i in range(1, n):
+                    c = (i - 1) % 7
+                    xt = np.float32(tau + c / h - 3 * LN2 + math.log(6.0))
+                    step = (i - 1) // 7 - 2   # -2..+2 ulps
+                    v = xt
+                    for _ in range(abs(step)):
+                        v = np.nextafter(v, np.float32(np.inf if step > 0 else -np.inf))
+                    x[r, t0 + i] = min(v, np.float32(0.0))
+            elif kind == 1:     # block maxima at and around k boundaries
+                j = -3 - (b % 20)
+                Mb = np.float32(j * LN2 - math.log(2 / 9))
+                d = (r // 6 + b) % 5 - 2
+                for _ in range(abs(d)):
+                    Mb = np.nextafter(Mb, np.float32(np.inf if d > 0 else -np.inf))
+                x[r, t0] = min(Mb, np.float32(0.0))
+            elif kind == 2:     # masked keys
+                mask = rng.random(n) < 0.5
+                x[r, t0:t0 + n][mask] = -np.inf
+                if b % 3 == 0:
+                    x[r, t0:t0 + n] = -np.inf
+            elif kind == 3:     # denormals and tiny values
+                x[r, t0:t0 + n] = -rng.uniform(0, 1e-37, n).astype(np.float32)
+                x[r, t0 + 1] = -np.float32(1e-42)
+            elif kind == 4:     # block maximum below the E8M0 range
+                x[r, t0:t0 + n] -= np.float32(80 + (b % 10))
+    return x
+
+
+def unpack(codes_u8: np.ndarray) -> np.ndarray:
+    c = codes_u8.astype(np.uint8)
+    return np.stack([c & 0xF, c >> 4], axis=-1).reshape(*c.shape[:-1], -1)
+
+
+@pytest.mark.parametrize("kind,params", [("efq", (-3.06, 2.30)), ("efq", (-2.90, 2.00)),
+                                         ("efq", (-2.10, 2.70)), ("lut", None)])
+def test_pgen_bitexact(B, orc, kind, params):
+    rng = np.random.default_rng(1)
+    mode = orc.LUT_MODE if kind == "lut" else orc.EFQ
+    tau, h = orc.LUT if kind == "lut" else params
+    for rows, cols in [(96, 200), (37, 64), (5, 1000), (64, 31)]:
+        x = adversarial_scores(rng, rows, cols, tau, h)
+        cg, eg = B.pgen(torch.from_numpy(x).cuda(), kind, (tau, h))
+        cg = unpack(cg.cpu().numpy())[:, :cols]
+        co, eo = orc.pgen(x, mode, tau, h)
+        assert np.array_equal(eg.cpu().numpy(), eo), (rows, cols)
+        assert np.array_equal(cg, co), (rows, cols, np.argwhere(cg != co)[:5])
+
+
+def test_pgen_random_bitexact(B, orc):
+    rng = np.random.default_rng(2)
+    x = -rng.exponential(3.0, size=(4096, 512)).astype(np.float32)
+    x[:, ::97] = 0.0
+    xg = torch.from_numpy(x).cuda()
+    cg, eg = B.pgen(xg, "efq")
+    co, eo = orc.pgen(x)
+    assert np.array_equal(eg.cpu().numpy(), eo)
+    assert np.array_equal(unpack(cg.cpu().numpy()), co)
+
+
+def test_pgen_expq_close(B, orc):
+    """Exp-then-quantize: the GPU's exp is not correctly rounded, so codes may
+    differ at round-to-nearest midpoints only."""
+    rng = np.random.default_rng(3)
+    x = -rng.exponential(3.0, size=(2048, 256)).astype(np.float32)
+    x[:, ::32] = np.minimum(x[:, ::32], -1e-3)
+    cg, eg = B.pgen(torch.from_numpy(x).cuda(), "expq")
+    co, eo = orc.pgen(x, orc.EXPQ)
+    cg = unpack(cg.cpu().numpy())
+    assert np.mean(eg.cpu().numpy() == eo) > 0.9999
+    assert np.mean(cg == co) > 0.9999
+
+
+@pytest.mark.parametrize("S,H,D", [(75, 3, 128), (256, 1, 64), (200, 2, 128)])
+def test_vquant_bitexact(B, orc, S, H, D):
+    g = torch.Generator().manual_seed(S + D)
+    v = torch.randn(2, S, H, D, generator=g) * torch.exp2(torch.randint(-30, 30, (1, 1, H, D), generator=g).float())
+    v[0, :5, 0, :3] = 0.0
+    v[1, :, H - 1, 5] = 0.0
+    v[1, 7, 0, 0] = -1e-39
+    v[0, 1, 0, 1] = -0.0
+    vb = v.to(torch.bfloat16)
+    vh = B.quant_v(vb.cuda())
+    sh = B.Shape(2, 1, S, H, H, D)
+    cg, eg = B.vhat_natural(vh, sh)
+    co, eo = orc.quant_v(orc.bf16_bits(vb))
+    nblk = (S + 31) // 32
+    assert np.array_equal(eg[:, :, :nblk].cpu().numpy(), eo)
+    assert np.array_equal(cg[:, :, :nblk * 32].cpu().numpy(), co)
+    # padding blocks are zero
+    assert int(cg[:, :, nblk * 32:].abs().sum()) == 0
+    assert int(eg[:, :, nblk:].sum()) == 0
+
+
+CASES = [
+    # (batch, seq_q, seq_k, heads_q, heads_kv, head_dim, causal)
+    (1, 256, 256, 2, 1, 64, False),
+    (1, 200, 200, 4, 2, 128, True),
+    (2, 75, 75, 2, 1, 128, False),
+    (1, 100, 300, 2, 2, 64, False),
+    (1, 333, 333, 1, 1, 128, True),
+]
+
+
+@pytest.mark.parametrize("case", CASES)
+@pytest.mark.parametrize("kind", ["efq", "lut"])
+def test_attn_dump_exact_scores(B, orc, case, kind):
+    """Exact-score inputs: every Q.K partial sum is exact, so the fused
+    kernel and the oracle see identical scores; codes and scales must match
+    bit for bit, the output within tolerance."""
+    Bt, Sq, Sk, Hq, Hkv, D, causal = case
+    w = inputs.Workload("d", Bt, Hq, Hkv, max(Sq, Sk), D, causal, "dyadic", 11 + Sq)
+    q, k, v = inputs.dyadic_qkv(w)
+    q, k, v = q[:, :Sq].contiguous(), k[:, :Sk].contiguous(), v[:, :Sk].contiguous()
+    mode = orc.LUT_MODE if kind == "lut" else orc.EFQ
+    vh = B.quant_v(v.cuda(), seq_q=Sq, heads_q=Hq)
+    out, codes, e8, rm, rl = B.attn_fwd_dump(q.cuda(), k.cuda(), vh, w.scale, causal, kind)
+    oo, co, eo, mo, lo = orc.attn(orc.bf16_bits(q), orc.bf16_bits(k), orc.bf16_bits(v), w.scale,
+                                  causal, mode, bc=64, dump=True)
+    nblk = (Sk + 31) // 32
+    cg = unpack(codes.cpu().numpy()).reshape(-1, nblk * 32)
+    assert np.array_equal(e8.cpu().numpy().reshape(-1, nblk), eo)
+    assert np.array_equal(cg, co)
+    assert np.array_equal(rm.cpu().numpy().ravel(), mo)
+    assert np.allclose(rl.cpu().numpy().ravel(), lo, rtol=1e-5)
+    og = out.cpu().numpy().transpose(0, 2, 1, 3).reshape(-1, D)
+    assert np.max(np.abs(og - oo)) <= TOL
+
+
+@pytest.mark.parametrize("case", CASES[:3])
+def test_attn_expq_exact_scores(B, orc, case):
+    Bt, Sq, Sk, Hq, Hkv, D, causal = case
+    w = inputs.Workload("d", Bt, Hq, Hkv, max(Sq, Sk), D, causal, "dyadic", 21 + Sq)
+    q, k, v = inputs.dyadic_qkv(w)
+    vh = B.quant_v(v.cuda(), seq_q=Sq, heads_q=Hq)
+    out, codes, e8, rm, rl = B.attn_fwd_dump(q.cuda(), k.cuda(), vh, w.scale, causal, "expq")
+    oo, co, eo, mo, lo = orc.attn(orc.bf16_bits(q), orc.bf16_bits(k), orc.bf16_bits(v), w.scale,
+                                  causal, orc.EXPQ, bc=64, dump=True)
+    nblk = (Sk + 31) // 32
+    cg = unpack(codes.cpu().numpy()).reshape(-1, nblk * 32)
+    assert np.mean(cg == co) > 1 - 1e-4
+    og = out.cpu().numpy().transpose(0, 2, 1, 3).reshape(-1, D)
+    assert np.max(np.abs(og - oo)) <= TOL
+
+
+def test_tiny_config_all_rows(B, orc):
+    """The tiny workload (1 x 256 x 64, N(0,1)), every row."""
+    w = inputs.WORKLOADS["tiny"]
+    q, k, v = inputs.make_qkv(w)
+    for kind, mode in [("efq", orc.EFQ), ("expq", orc.EXPQ), ("lut", orc.LUT_MODE)]:
+        out = B.attn_fwd(q.cuda(), k.cuda(), v.cuda(), w.scale, w.causal, kind)
+        oo = orc.attn(orc.bf16_bits(q), orc.bf16_bits(k), orc.bf16_bits(v), w.scale, w.causal, mode)
+        og = out.cpu().numpy().transpose(0, 2, 1, 3).reshape(-1, w.head_dim)
+        err = np.abs(og - oo).max(axis=1)
+        assert np.max(err) <= TOL, (kind, np.sort(err)[-5:])
+
+
+def test_entry_points_match_ex(B):
+    w = inputs.WORKLOADS["tiny"]
+    q, k, v = (t.cuda() for t in inputs.make_qkv(w))
+    a = B.efq_attn_fwd(q, k, v, w.scale, False)
+    b = B.attn_fwd(q, k, v, w.scale, False, "efq")
+    c = B.efq_attn_fwd_expq(q, k, v, w.scale, False)
+    d = B.attn_fwd(q, k, v, w.scale, False, "expq")
+    assert torch.equal(a, b) and torch.equal(c, d)
+
+
+def test_same_operand_v_constant(B):
+    """V = 1 makes O = 1: P~V and P~1 share one operand (Sec. III-A)."""
+    w = inputs.Workload("c", 1, 4, 2, 1000, 128, True, "qwen", 5)
+    q, k, v = inputs.make_qkv(w)
+    for c in (1.0, -3.0):
+        vc = torch.full_like(v, c)
+        for kind in ("efq", "expq", "lut"):
+            out = B.attn_fwd(q.cuda(), k.cuda(), vc.cuda(), w.scale, True, kind)
+            assert float((out - c).abs().max()) <= 1e-6 * abs(c) * 8
