@@ -97,7 +97,8 @@ enum efq_status {
  * even with saturation, sign bit = sign of the bf16 input).  Layout, with
  * nb = 2 * ceil(seq_k / 64) key blocks (blocks past seq_k hold zeros):
  *   codes  [batch][heads_kv][nb][head_dim][16 bytes]  32 keys per 16 bytes
- *   scales [batch][heads_kv][nb][head_dim]            E8M0 bytes
+ *   scales [batch][heads_kv][nb][32][head_dim/32]     E8M0 bytes, column d
+ *                                                     at [d % 32][d / 32]
  * The scales start at byte offset efq_vhat_scale_offset(s).  Within the 16
  * code bytes the 32 keys are stored in the order the FP4 matrix core reads
  * them: key t of the block sits in nibble e(t) = 8*(2*((t>>2)&1) + (t>>4))

@@ -260,5 +260,7 @@ def vhat_natural(vhat: torch.Tensor, shape: Shape):
     e = (8 * (2 * ((t >> 2) & 1) + (t >> 4)) + 4 * ((t >> 3) & 1) + (t & 3)).to(vhat.device)
     keyed = nib[..., e]                                # [..., 32] key order
     codes_nat = keyed.permute(0, 1, 2, 4, 3).reshape(B, H, nb * 32, D)
-    e8 = vhat[off: off + B * H * nb * D].view(B, H, nb, D)
+    # scale plane: byte (d % 32) * (D / 32) + d / 32 of each block
+    e8 = vhat[off: off + B * H * nb * D].view(B, H, nb, 32, D // 32)
+    e8 = e8.permute(0, 1, 2, 4, 3).reshape(B, H, nb, D)
     return codes_nat, e8

@@ -37,6 +37,12 @@ def build(verbose: bool = False, extra=()) -> str:
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
         raise RuntimeError("hipcc failed building libefq_attn.so")
+    # every kernel's host stub must be defined, or dlopen fails later
+    nm = subprocess.run(["nm", "-D", "--undefined-only", tmp], capture_output=True, text=True)
+    missing = [ln for ln in nm.stdout.splitlines() if "__device_stub__" in ln]
+    if missing:
+        os.remove(tmp)
+        raise RuntimeError("kernel host stubs missing from the build:\n" + "\n".join(missing[:5]))
     os.replace(tmp, LIB)
     return LIB
 

@@ -27,6 +27,8 @@
 #include <cstdio>
 #include <cstring>
 #include <mutex>
+#include <type_traits>
+#include <utility>
 
 #include "efq_attn.h"
 
@@ -49,6 +51,9 @@ constexpr int kWaves = 4;      // waves per workgroup
 constexpr int kBr = kWaveQ * kWaves;  // queries per workgroup
 constexpr int kBc = 64;        // keys per tile (two 32-key microscaling blocks)
 constexpr int kThreads = 64 * kWaves;
+#ifndef EFQ_WAVES_PER_SIMD
+#define EFQ_WAVES_PER_SIMD 2   // fused-kernel occupancy target (register budget)
+#endif
 
 // C16 fold table of EFQ-Softmax-LUT (Sec. II-D), nibble j = C16[j].
 constexpr unsigned long long kC16 = 0x7765543322111110ull;
@@ -77,15 +82,6 @@ __device__ __forceinline__ void swap32f(float& a, float& b) {
   b = __uint_as_float(ub);
 }
 
-// Pack eight codes c_e - 1 (each in [-1, 6]) into eight nibbles c_e, nibble
-// e = element e: Horner on (c - 1), then one add of 0x11111111.
-__device__ __forceinline__ unsigned pack8m1(const int* cm1) {
-  unsigned p = (unsigned)cm1[7];
-#pragma unroll
-  for (int e = 6; e >= 0; --e) p = (p << 4) + (unsigned)cm1[e];
-  return p + 0x11111111u;
-}
-
 __device__ __forceinline__ float max16(const f32x16& v) {
   float m = v[0];
 #pragma unroll
@@ -107,10 +103,19 @@ __host__ __device__ __forceinline__ int key_nibble(int t) {
 
 // -------------------------------------------------- probability stage
 // Input: the two 32x32 score accumulators of a wave (s0: keys 0..31, s1: keys
-// 32..63 of the tile; -inf where masked), the running maximum m (score units,
-// per lane = per query).  Output: the FP4 B operand (4 dwords, 32 codes of
-// the lane's block), the lane's E8M0 scale, alpha = exp(m_old - m_new), and
+// 32..63 of the tile; -inf where masked), the running maximum m (per lane =
+// per query).  Output: the FP4 B operand (4 dwords, the 32 codes of the
+// lane's own block), the lane's E8M0 scale, alpha = exp(m_old - m_new), and
 // m updated to m_new (Eq. rowmax-update).
+//
+// The stage is split into pieces so the fused kernel can interleave them
+// with the matrix-core work of the next tile:
+//   pg_max     partial block maxima of the lane's 32 scores
+//   pg_params  row maximum, alpha, and the per-block parameters (Alg. 1:
+//              M_b, k_b, and the affine bias; or the exp-then-quantize scale)
+//   pg_pair<E> codes of elements E, E+1 (element e = 16 * window + register)
+//   pg_finish  one v_permlane32_swap per half-block: lane L keeps window L/32
+// pgen<KIND>() runs them in order (standalone kernel and probe).
 struct PgenArgs {
   float scale;   // softmax scale
   float sh;      // fl(scale * h)
@@ -125,136 +130,154 @@ struct PgenOut {
   float alpha;
 };
 
-// Row maximum, block maxima, alpha: shared by every policy.
-// `unit` converts raw dot products to the units m is kept in: the softmax
-// scale (natural-log units) or scale * log2 e (log2 units, LOG2 = true).
-// Returns bmine = raw-dot maximum of the lane's own 32-key block (window
-// lane/32), updates m.
-template <bool LOG2>
-__device__ __forceinline__ float row_block_max(const f32x16& s0, const f32x16& s1, float& m,
-                                               float unit, float& alpha) {
-  float pm0 = max16(s0), pm1 = max16(s1);
-  swap32f(pm0, pm1);                         // lower: (own pm0, partner pm0); upper: (partner pm1, own pm1)
-  float bmine = __builtin_fmaxf(pm0, pm1);   // block maximum of this lane's window
-  float t0 = bmine, t1 = bmine;
-  swap32f(t0, t1);                           // (block 0 max, block 1 max) in every lane
-  float rmax = __builtin_fmaxf(t0, t1);
-  float mt = rmax * unit;                    // rowmax S^j (raw max times scale; monotone)
-  float mnew = __builtin_fmaxf(m, mt);
-  // alpha = exp(m^{j-1} - m^j), Eq. (alpha); exactly 1 when the max is unchanged
-  const float d = LOG2 ? (m - mnew) : (m - mnew) * kInvLn2;
-  alpha = (m == mnew) ? 1.0f : __builtin_amdgcn_exp2f(d);
-  m = mnew;
-  return bmine;
+struct PgenState {
+  float bias[2];      // EFQ/LUT: -(m + k_b log2 + log6 + tau) h per window
+  float sc[2];        // EXPQ: 2^k_b per window (fp32 scale of the conversion)
+  float mq;           // EXPQ: running maximum in log2 units
+  int scale_b;        // E8M0 of the lane's own block
+  float alpha;
+  unsigned w[4];      // packed codes: window 0 regs 0-7, 8-15, window 1 ...
+};
+
+template <int SH>
+__device__ __forceinline__ unsigned lshl_add_imm(int v, unsigned acc) {
+  unsigned r;
+  asm("v_lshl_add_u32 %0, %1, %2, %3" : "=v"(r) : "v"(v), "n"(SH), "v"(acc));
+  return r;
 }
 
-// Alg. 1 for both 32-key blocks of the lane's query, codes for the lane's 32
-// scores, then the swap that gives every lane its own block.
-template <bool LUT>
-__device__ __forceinline__ PgenOut pgen_efq(const f32x16& s0, const f32x16& s1, float& m,
-                                            const PgenArgs& pa) {
-  PgenOut o;
-  float bmine = row_block_max<false>(s0, s1, m, pa.scale, o.alpha);
-  // M_b = max_t x_t = fl(fl(max acc * scale) - m)
-  float Mb = bmine * pa.scale - m;
-  // k_b = floor((M_b + log(2/9)) / log 2), Eq. (k-rule); -inf -> INT_MIN -> -127
-  int kb = cvt_flr((Mb + kLog29) * kInvLn2);
-  kb = kb < -127 ? -127 : kb;
-  // z_t - tau = x_t - (k_b log2 + log6 + tau): fold into bias = -(m + off) h
-  float off = (float)kb * kLn2 + pa.c;
-  float bias = (m + off) * pa.negh;
-  float b0 = bias, b1 = bias;
-  swap32f(b0, b1);                           // (bias of block 0, bias of block 1)
-  o.scale_b = kb + 127;
+template <int KIND>
+__device__ __forceinline__ void pg_max(const f32x16& s0, const f32x16& s1, float& pm0, float& pm1) {
+  if constexpr (KIND == EFQ_PGEN_NOOP) {
+    pm0 = pm1 = 0.0f;
+  } else {
+    pm0 = max16(s0);
+    pm1 = max16(s1);
+  }
+}
 
-  unsigned w[4];                              // W0lo, W0hi, W1lo, W1hi
-#pragma unroll
-  for (int half = 0; half < 4; ++half) {
-    const f32x16& s = half < 2 ? s0 : s1;
-    const float bb = half < 2 ? b0 : b1;
-    int cm1[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      // u = (z_t - tau) h, Eq. (d8-index); c - 1 = clip(floor(u), -1, 6)
-      float u = __builtin_fmaf(s[(half & 1) * 8 + e], pa.sh, bb);
-      int f = cvt_flr(u);
-      if (LUT) {
-        int j = clampi(f, -1, 14) + 1;         // j16 in 0..15
-        cm1[e] = (int)((kC16 >> (4 * j)) & 0xF) - 1;
-      } else {
-        cm1[e] = clampi(f, -1, 6);
-      }
+template <int KIND>
+__device__ __forceinline__ void pg_params(float pm0, float pm1, float& m, const PgenArgs& pa,
+                                          PgenState& st) {
+  if constexpr (KIND == EFQ_PGEN_NOOP) {
+    st.scale_b = 127 - 6;
+    st.alpha = 1.0f;
+    st.w[0] = st.w[1] = st.w[2] = st.w[3] = 0x22222222u;
+    return;
+  } else {
+    constexpr bool LOG2 = (KIND == EFQ_PGEN_EXPQ);
+    const float unit = LOG2 ? pa.l2s : pa.scale;
+    swap32f(pm0, pm1);                          // lower: (own, partner) block 0; upper: block 1
+    const float bmine = __builtin_fmaxf(pm0, pm1);   // raw maximum of the lane's own block
+    float t0 = bmine, t1 = bmine;
+    swap32f(t0, t1);                            // (block 0 max, block 1 max) in every lane
+    const float mt = __builtin_fmaxf(t0, t1) * unit;   // rowmax S^j (monotone in the raw max)
+    const float mnew = __builtin_fmaxf(m, mt);
+    // alpha = exp(m^{j-1} - m^j), Eq. (alpha); exactly 1 when the max is unchanged
+    const float d = LOG2 ? (m - mnew) : (m - mnew) * kInvLn2;
+    st.alpha = (m == mnew) ? 1.0f : __builtin_amdgcn_exp2f(d);
+    m = mnew;
+    if constexpr (KIND == EFQ_PGEN_EXPQ) {
+      // exp-then-quantize, Eq. (post-softmax-path): max_t exp(x_t) =
+      // exp(max_t x_t); the shift S2 - m2 is exact at the row maximum, so it
+      // gets p = 1 exactly (an fma of the unshifted score could land on the
+      // wrong side of the power-of-two scale boundary)
+      const float amax = __builtin_amdgcn_exp2f(bmine * pa.l2s - m);
+      int kb = (int)((__float_as_uint(amax) >> 23) & 0xFF) - 127 - 2;
+      kb = kb < -126 ? -126 : kb;               // 2^k must be a normal fp32 scale
+      unsigned k0 = (unsigned)(kb + 127), k1 = k0;
+      swap32(k0, k1);                           // (E8M0 of block 0, of block 1)
+      st.sc[0] = __uint_as_float(k0 << 23);
+      st.sc[1] = __uint_as_float(k1 << 23);
+      st.scale_b = amax > 0.0f ? kb + 127 : 0;  // no visible key: E8M0 0x00, codes 0
+      st.mq = m;
+      st.w[0] = st.w[1] = st.w[2] = st.w[3] = 0u;
+    } else {
+      // Alg. 1: M_b = max_t x_t = fl(fl(max acc * scale) - m)
+      const float Mb = bmine * pa.scale - m;
+      // k_b = floor((M_b + log(2/9)) / log 2), Eq. (k-rule); -inf -> INT_MIN -> -127
+      int kb = cvt_flr((Mb + kLog29) * kInvLn2);
+      kb = kb < -127 ? -127 : kb;
+      // (z_t - tau) h with z_t = x_t - k_b log2 - log6 (Eq. z-def), folded to
+      // fma(acc, scale h, bias), bias = -(m + k_b log2 + log6 + tau) h
+      const float off = (float)kb * kLn2 + pa.c;
+      float b0 = (m + off) * pa.negh, b1 = b0;
+      swap32f(b0, b1);                          // (bias of block 0, bias of block 1)
+      st.bias[0] = b0;
+      st.bias[1] = b1;
+      st.scale_b = kb + 127;
+      // packed codes start at 0x11111111: each element adds (c - 1) << 4e
+      st.w[0] = st.w[1] = st.w[2] = st.w[3] = 0x11111111u;
     }
-    w[half] = pack8m1(cm1);
   }
-  swap32(w[0], w[2]);
-  swap32(w[1], w[3]);
-  o.bop = u32x4{w[0], w[1], w[2], w[3]};
+}
+
+// Code minus one of one score: u = (z_t - tau) h, Eq. (d8-index), and
+// c - 1 = clip(floor(u), -1, 6); for EFQ-Softmax-LUT the 16-level index
+// j16 = clip(floor(u) + 1, 0, 15) folded through C16 (Sec. II-D).
+template <int KIND>
+__device__ __forceinline__ int pg_code_m1(float acc, const PgenArgs& pa, float bias) {
+  const float u = __builtin_fmaf(acc, pa.sh, bias);
+  const int f = cvt_flr(u);
+  if constexpr (KIND == EFQ_PGEN_LUT) {
+    const int j = clampi(f, -1, 14) + 1;
+    return (int)((kC16 >> (4 * j)) & 0xF) - 1;
+  } else {
+    return clampi(f, -1, 6);
+  }
+}
+
+// Codes of elements E and E+1 (same window, same dword).
+template <int KIND, int E>
+__device__ __forceinline__ void pg_pair(const f32x16& s0, const f32x16& s1, const PgenArgs& pa,
+                                        PgenState& st) {
+  if constexpr (KIND != EFQ_PGEN_NOOP) {
+    constexpr int WIN = E / 16, R = E % 16, DW = E / 8, NIB = E % 8;
+    const f32x16& s = WIN ? s1 : s0;
+    if constexpr (KIND == EFQ_PGEN_EXPQ) {
+      const float p0 = __builtin_amdgcn_exp2f(s[R] * pa.l2s - st.mq);
+      const float p1 = __builtin_amdgcn_exp2f(s[R + 1] * pa.l2s - st.mq);
+      // RNE(p / 2^k) to E2M1 with saturation, two codes into byte NIB/2
+      st.w[DW] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(st.w[DW], p0, p1, st.sc[WIN], NIB / 2);
+    } else {
+      st.w[DW] = lshl_add_imm<4 * NIB>(pg_code_m1<KIND>(s[R], pa, st.bias[WIN]), st.w[DW]);
+      st.w[DW] = lshl_add_imm<4 * NIB + 4>(pg_code_m1<KIND>(s[R + 1], pa, st.bias[WIN]), st.w[DW]);
+    }
+  }
+}
+
+template <int KIND>
+__device__ __forceinline__ PgenOut pg_finish(PgenState& st) {
+  PgenOut o;
+  if constexpr (KIND != EFQ_PGEN_NOOP) {
+    swap32(st.w[0], st.w[2]);
+    swap32(st.w[1], st.w[3]);
+  }
+  o.bop = u32x4{st.w[0], st.w[1], st.w[2], st.w[3]};
+  o.scale_b = st.scale_b;
+  o.alpha = st.alpha;
   return o;
 }
 
-// Exp-then-quantize baseline, Eq. (post-softmax-path): p = exp(x) in fp32,
-// block scale 2^(floor(log2 max p) - 2), RNE E2M1 with saturation.  The
-// running maximum is kept in log2 units and the shift x2 = fl(S2 - m2) is
-// exact at the row maximum, so that element gets p = 1 exactly (an fma of
-// the unshifted score would leave it at 1 -/+ 1 ulp, on the wrong side of
-// the power-of-two scale boundary half of the time).
-__device__ __forceinline__ PgenOut pgen_expq(const f32x16& s0, const f32x16& s1, float& m,
-                                             const PgenArgs& pa) {
-  PgenOut o;
-  float bmine = row_block_max<true>(s0, s1, m, pa.l2s, o.alpha);
-  // max_t exp(x_t) = exp(max_t x_t): one exponential per block
-  const float amax = __builtin_amdgcn_exp2f(bmine * pa.l2s - m);
-  const int e = (int)((__float_as_uint(amax) >> 23) & 0xFF);   // biased exponent
-  int kb = e - 127 - 2;
-  kb = kb < -126 ? -126 : kb;                // 2^k must be a normal fp32 scale
-  unsigned k0 = (unsigned)(kb + 127), k1 = k0;
-  swap32(k0, k1);                            // (E8M0 of block 0, of block 1)
-  const float sc0 = __uint_as_float(k0 << 23);   // 2^k as an fp32 scale
-  const float sc1 = __uint_as_float(k1 << 23);
-  o.scale_b = amax > 0.0f ? kb + 127 : 0;    // no visible key: E8M0 0x00, codes 0
-  unsigned w[4];
-#pragma unroll
-  for (int half = 0; half < 4; ++half) {
-    const f32x16& s = half < 2 ? s0 : s1;
-    const float sc = half < 2 ? sc0 : sc1;
-    float p[8];
-#pragma unroll
-    for (int e2 = 0; e2 < 8; ++e2)
-      p[e2] = __builtin_amdgcn_exp2f(s[(half & 1) * 8 + e2] * pa.l2s - m);
-    // RNE(p / 2^k) to E2M1 with saturation, two codes per byte
-    unsigned word = 0;
-    word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, p[0], p[1], sc, 0);
-    word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, p[2], p[3], sc, 1);
-    word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, p[4], p[5], sc, 2);
-    word = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(word, p[6], p[7], sc, 3);
-    w[half] = word;
+template <int KIND, int E0, int E1>
+__device__ __forceinline__ void pg_pairs(const f32x16& s0, const f32x16& s1, const PgenArgs& pa,
+                                         PgenState& st) {
+  if constexpr (E0 < E1) {
+    pg_pair<KIND, E0>(s0, s1, pa, st);
+    pg_pairs<KIND, E0 + 2, E1>(s0, s1, pa, st);
   }
-  swap32(w[0], w[2]);
-  swap32(w[1], w[3]);
-  o.bop = u32x4{w[0], w[1], w[2], w[3]};
-  return o;
-}
-
-// Timing control: a constant operand and no probability-stage work.
-__device__ __forceinline__ PgenOut pgen_noop(const f32x16& s0, const f32x16& s1, float& m,
-                                             const PgenArgs& pa) {
-  PgenOut o;
-  o.bop = u32x4{0x22222222u, 0x22222222u, 0x22222222u, 0x22222222u};
-  o.scale_b = 127 - 6;
-  o.alpha = 1.0f;
-  m = 0.0f;
-  (void)s0; (void)s1; (void)pa;
-  return o;
 }
 
 template <int KIND>
 __device__ __forceinline__ PgenOut pgen(const f32x16& s0, const f32x16& s1, float& m,
                                         const PgenArgs& pa) {
-  if constexpr (KIND == EFQ_PGEN_EFQ) return pgen_efq<false>(s0, s1, m, pa);
-  else if constexpr (KIND == EFQ_PGEN_LUT) return pgen_efq<true>(s0, s1, m, pa);
-  else if constexpr (KIND == EFQ_PGEN_EXPQ) return pgen_expq(s0, s1, m, pa);
-  else return pgen_noop(s0, s1, m, pa);
+  float pm0, pm1;
+  PgenState st;
+  pg_max<KIND>(s0, s1, pm0, pm1);
+  pg_params<KIND>(pm0, pm1, m, pa, st);
+  pg_pairs<KIND, 0, 32>(s0, s1, pa, st);
+  if constexpr (KIND == EFQ_PGEN_NOOP) asm volatile("" ::"v"(s0), "v"(s1));   // keep Q K^T live
+  return pg_finish<KIND>(st);
 }
 
 // Operand codes of a lane in key order: 16 bytes, key 2j low nibble of byte j.
@@ -346,7 +369,8 @@ __global__ __launch_bounds__(256) void vquant_kernel(const unsigned short* __res
       words[e >> 3] |= code << (4 * (e & 7));
     }
     *(u32x4*)(codes + (long)(d0 + c) * 16) = u32x4{words[0], words[1], words[2], words[3]};
-    scales[d0 + c] = (uint8_t)(k + 127);
+    const int d = d0 + c;
+    scales[(d & 31) * (a.D >> 5) + (d >> 5)] = (uint8_t)(k + 127);
   }
 }
 
@@ -366,67 +390,110 @@ struct AttnArgs {
   int nblk;           // ceil(Sk / 32)
 };
 
+// LDS layout.  A K tile is stored in the order the bf16 MFMA reads its A
+// operand: 1 KB blocks, one per (32-key window w, 16-column step kk), slot
+// `lane` of block (w, kk) holding K[32w + lane%32][16kk + 8(lane/32) .. +8].
+// Every operand read is then one contiguous 1 KB wave access (no bank
+// conflicts, immediate offsets), and every block is filled by one
+// global_load_lds_dwordx4 (LDS address = base + 16 * lane).  A V~ tile (two
+// 32-key blocks) is stored as in global memory: codes, then E8M0 scales
+// grouped per lane (byte (d % 32) * (D/32) + d / 32 of each block).
+// K and V~ have three buffers each: step j reads K of tile j+1 and V~ of
+// tile j while K of tile j+3 and V~ of tile j+2 stream in, so a load has
+// two steps to land.
+constexpr int kStages = 3;
 template <int D>
 struct Smem {
-  static constexpr int kRow = D * 2 + 16;                // padded K row (bytes)
-  static constexpr int kK = kBc * kRow;                  // K tile
+  static constexpr int kK = kBc * D * 2;                 // one K tile
   static constexpr int kVc = 2 * D * 16;                 // V~ codes of two blocks
-  static constexpr int kVs = 2 * D;                      // V~ scales of two blocks
-  static constexpr int kStage = kK + kVc + kVs;
-  static constexpr int kTotal = 2 * kStage;
+  static constexpr int kVs = 256;                        // V~ scales (2 D bytes, padded)
+  static constexpr int kV = kVc + kVs;                   // one V~ tile
+  static constexpr int kKOff = 0;
+  static constexpr int kVOff = kStages * kK;
+  static constexpr int kTotal = kStages * (kK + kV);
 };
 
-template <int D>
-struct TileRegs {
-  // global -> register staging of one K/V~ tile, spread over the workgroup
-  static constexpr int kKChunks = kBc * D / 8;           // 16-byte chunks of K
-  static constexpr int kKPer = kKChunks / kThreads;      // per thread
-  static constexpr int kVChunks = 2 * D;                 // 16-byte chunks of V~ codes
-  static constexpr int kVPer = (kVChunks + kThreads - 1) / kThreads;
-  u32x4 k[kKPer];
-  u32x4 vc[kVPer];
-  unsigned vs;                                           // 4 scale bytes
-};
-
-template <int D>
-__device__ __forceinline__ void load_tile(TileRegs<D>& tr, const unsigned short* __restrict__ kp,
-                                          const uint8_t* __restrict__ vcodes,
-                                          const uint8_t* __restrict__ vscales, int key0, int Sk,
-                                          long kstride) {
-  const int tid = threadIdx.x;
-#pragma unroll
-  for (int i = 0; i < TileRegs<D>::kKPer; ++i) {
-    int c = tid + i * kThreads;
-    int row = c / (D / 8), col = c % (D / 8);
-    int key = key0 + row;
-    if (key < Sk)
-      tr.k[i] = *(const u32x4*)(kp + (long)key * kstride + col * 8);
-    else
-      tr.k[i] = u32x4{0, 0, 0, 0};
-  }
-#pragma unroll
-  for (int i = 0; i < TileRegs<D>::kVPer; ++i) {
-    int c = tid + i * kThreads;
-    if (c < TileRegs<D>::kVChunks) tr.vc[i] = *(const u32x4*)(vcodes + (long)c * 16);
-  }
-  if (tid < 2 * D / 4) tr.vs = *(const unsigned*)(vscales + tid * 4);
+// Direct-to-LDS loads (buffer_load ... lds: LDS address = M0 base + size *
+// lane).  The buffer resource's range check returns zeros past the end of
+// K, so keys beyond seq_k need no special case (they are masked anyway).
+// The per-lane byte offsets are loop invariant; the tile position goes in
+// the scalar offset.  Asynchronous: the caller waits on vmcnt before the
+// workgroup barrier that publishes the tile.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, unsigned bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
 template <int D>
-__device__ __forceinline__ void store_tile(const TileRegs<D>& tr, uint8_t* stage) {
-  const int tid = threadIdx.x;
-#pragma unroll
-  for (int i = 0; i < TileRegs<D>::kKPer; ++i) {
-    int c = tid + i * kThreads;
-    int row = c / (D / 8), col = c % (D / 8);
-    *(u32x4*)(stage + row * Smem<D>::kRow + col * 16) = tr.k[i];
+struct KLoad {
+  static constexpr int KK = D / 16;
+  static constexpr int PER = 2 * KK / kWaves;            // 1 KB blocks per wave
+  static_assert(KK % PER == 0, "a wave's blocks share one 32-key window");
+  const void* base;
+  unsigned bytes;
+  int voff0;                                             // lane's byte offset, first block
+  unsigned tile_bytes;                                   // bytes per 64 keys
+  __device__ void init(const unsigned short* kbatch, int Sk, int Hkv, int g, int wave, int lane) {
+    base = kbatch;
+    bytes = (unsigned)((long)Sk * Hkv * D * 2);
+    tile_bytes = (unsigned)(kBc * Hkv * D * 2);
+    // the wave's blocks are (window w, k-steps kk0 .. kk0+PER-1): block i
+    // sits 32 bytes (16 bf16 columns) after block i-1 in every row
+    const int blk = wave * PER;
+    const int w = blk / KK, kk0 = blk % KK;
+    const int row = 32 * w + (lane & 31);
+    voff0 = ((row * Hkv + g) * D + kk0 * 16 + (lane >> 5) * 8) * 2;
   }
+  static constexpr int kIssued = PER;                    // loads per wave per tile
+  __device__ void issue(uint8_t* kbuf, int tile, int wave) const {
+    const auto rsrc = make_rsrc(base, bytes);
 #pragma unroll
-  for (int i = 0; i < TileRegs<D>::kVPer; ++i) {
-    int c = tid + i * kThreads;
-    if (c < TileRegs<D>::kVChunks) *(u32x4*)(stage + Smem<D>::kK + c * 16) = tr.vc[i];
+    for (int i = 0; i < PER; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, kbuf + (wave * PER + i) * 1024, 16,
+                                               voff0 + 32 * i, (int)(tile * tile_bytes), 0, 0);
   }
-  if (tid < 2 * D / 4) *(unsigned*)(stage + Smem<D>::kK + Smem<D>::kVc + tid * 4) = tr.vs;
+};
+
+template <int D>
+struct VLoad {
+  static constexpr int NB = Smem<D>::kVc / 1024;          // 1 KB code blocks (2 or 4)
+  const uint8_t* codes;
+  const uint8_t* scales;
+  int nb;
+  __device__ void init(const uint8_t* vcodes, const uint8_t* vscales, int nblocks) {
+    codes = vcodes;
+    scales = vscales;
+    nb = nblocks;
+  }
+  // loads a wave issues per tile
+  __device__ static int issued(int wave) { return (wave < NB ? 1 : 0) + (wave == kWaves - 1 ? 1 : 0); }
+  __device__ void issue(uint8_t* vbuf, int tile, int wave, int lane) const {
+    const auto rc = make_rsrc(codes, (unsigned)(nb * D * 16));
+    const auto rs = make_rsrc(scales, (unsigned)(nb * D));
+    if (wave < NB)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, vbuf + wave * 1024, 16, lane * 16,
+                                               tile * 2 * D * 16 + wave * 1024, 0, 0);
+    if (wave == kWaves - 1) {
+      // 2 D scale bytes as dwords; for D = 64 the upper lanes repeat the
+      // lower ones into the padding
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, vbuf + Smem<D>::kVc, 4, (lane % (2 * D / 4)) * 4,
+                                               tile * 2 * D, 0, 0);
+    }
+  }
+};
+
+__device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// Wait until at most n vector-memory loads of this wave are outstanding
+// (loads complete in issue order); n is wave-uniform and at most 6.
+__device__ __forceinline__ void wait_vmem_le(int n) {
+  switch (n) {
+    case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+    case 1: asm volatile("s_waitcnt vmcnt(1)" ::: "memory"); break;
+    case 2: asm volatile("s_waitcnt vmcnt(2)" ::: "memory"); break;
+    case 3: asm volatile("s_waitcnt vmcnt(3)" ::: "memory"); break;
+    case 4: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
+    case 5: asm volatile("s_waitcnt vmcnt(5)" ::: "memory"); break;
+    default: asm volatile("s_waitcnt vmcnt(6)" ::: "memory"); break;
+  }
 }
 
 // Map a workgroup index to (batch, head, query tile).  Workgroups are handed
@@ -444,148 +511,313 @@ __device__ __forceinline__ void map_work(const AttnArgs& a, int& b, int& hq, int
   b = bh / a.Hq;
 }
 
+// S^T = K Q^T for one 64-key tile (two 32-key windows) from an LDS K tile,
+// with the LDS operand reads issued two steps ahead of their MFMAs.
+template <int D>
+__device__ __forceinline__ void qk_tile(const uint8_t* kbuf, const bf16x8* qreg, int lane,
+                                        f32x16& s0, f32x16& s1) {
+  constexpr int KK = D / 16;
+  const uint8_t* p0 = kbuf + lane * 16;                  // window 0 blocks
+  const uint8_t* p1 = p0 + KK * 1024;                    // window 1 blocks
+  bf16x8 a0[2], a1[2];
+  a0[0] = *(const bf16x8*)(p0);
+  a1[0] = *(const bf16x8*)(p1);
+  a0[1] = *(const bf16x8*)(p0 + 1024);
+  a1[1] = *(const bf16x8*)(p1 + 1024);
+  s0 = f32x16{};
+  s1 = f32x16{};
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[kk & 1], qreg[kk], s0, 0, 0, 0);
+    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[kk & 1], qreg[kk], s1, 0, 0, 0);
+    if (kk + 2 < KK) {
+      a0[kk & 1] = *(const bf16x8*)(p0 + (kk + 2) * 1024);
+      a1[kk & 1] = *(const bf16x8*)(p1 + (kk + 2) * 1024);
+    }
+  }
+}
+
+// V~ operands of one tile for the lane: the 16 code bytes of each slab and
+// the E8M0 scales of all slabs in one register (slab s = byte s).
+template <int D>
+struct VOps {
+  u32x4 a[D / 32];
+  int sv;
+};
+
+template <int D>
+__device__ __forceinline__ void read_v(const uint8_t* vb, int lane, VOps<D>& v) {
+  constexpr int NS = D / 32;
+  const int half = lane >> 5;
+  const uint8_t* vc = vb + (half * D + (lane & 31)) * 16;
+#pragma unroll
+  for (int s = 0; s < NS; ++s) v.a[s] = *(const u32x4*)(vc + s * 32 * 16);
+  const uint8_t* vsp = vb + Smem<D>::kVc + half * D + (lane & 31) * NS;
+  if constexpr (NS == 4) v.sv = *(const int*)vsp;
+  else v.sv = *(const unsigned short*)vsp;
+}
+
+// O^T slabs += V~^T P~^T on the FP4 MFMA.  The lane's E8M0 scales of all
+// slabs sit in one register `sv`; slab S selects byte S (op_sel).
+template <int NS, int S = 0, int D>
+__device__ __forceinline__ void pv_slabs(f32x16* oacc, const VOps<D>& v, const i32x8& bop, int sb) {
+  if constexpr (S < NS) {
+    const i32x8 aop = i32x8{(int)v.a[S][0], (int)v.a[S][1], (int)v.a[S][2], (int)v.a[S][3], 0, 0, 0, 0};
+    oacc[S] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(aop, bop, oacc[S], 4, 4, S, v.sv, 0, sb);
+    pv_slabs<NS, S + 1>(oacc, v, bop, sb);
+  }
+}
+
+// Mask keys past the end and, for causal attention, keys after the query
+// (the mask acts before the probability stage).  lim = number of visible
+// keys of this lane counted from the tile start.
+__device__ __forceinline__ void mask_tile(f32x16& s0, f32x16& s1, int lim, int half) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int kofs = 8 * (r >> 2) + 4 * half + (r & 3);
+    s0[r] = kofs < lim ? s0[r] : -INFINITY;
+    s1[r] = kofs + 32 < lim ? s1[r] : -INFINITY;
+  }
+}
+
+
+// Regions 1 .. KK-1 of the pipelined step (see step_next).
+template <int D, int KIND, int I>
+__device__ __forceinline__ void qk_regions(const uint8_t* p0, const uint8_t* p1, bf16x8* a0,
+                                           bf16x8* a1, const bf16x8* qreg, f32x16& sn0,
+                                           f32x16& sn1, const uint8_t* vb, int lane, VOps<D>& vop,
+                                           const f32x16& sc0, const f32x16& sc1,
+                                           const PgenArgs& pa, PgenState& st) {
+  constexpr int KK = D / 16;
+  if constexpr (I < KK) {
+    sn0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[I & 1], qreg[I], sn0, 0, 0, 0);
+    sn1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[I & 1], qreg[I], sn1, 0, 0, 0);
+    if constexpr (I + 2 < KK) {
+      a0[I & 1] = *(const bf16x8*)(p0 + (I + 2) * 1024);
+      a1[I & 1] = *(const bf16x8*)(p1 + (I + 2) * 1024);
+    }
+    if constexpr (I == KK - 1) read_v<D>(vb, lane, vop);
+    constexpr int P0 = 16 * (I - 1) / (KK - 1), P1 = 16 * I / (KK - 1);
+    pg_pairs<KIND, 2 * P0, 2 * P1>(sc0, sc1, pa, st);
+    __builtin_amdgcn_sched_barrier(0);
+    qk_regions<D, KIND, I + 1>(p0, p1, a0, a1, qreg, sn0, sn1, vb, lane, vop, sc0, sc1, pa, st);
+  }
+}
+
+// One software-pipelined step: the probability stage of tile j (scores sc)
+// interleaved, region by region, with S(j+1) = K(j+1) Q^T on the bf16 MFMA.
+// Each region holds one k-step (two MFMAs), the LDS operand reads of the
+// k-step two ahead, and a slice of VALU work; sched_barrier keeps the
+// regions in this order.  The V~ operands of tile j are read in the last
+// region (into the freed operand registers).
+template <int D, int KIND>
+__device__ __forceinline__ PgenOut step_next(const uint8_t* kb_next, const uint8_t* vb, const bf16x8* qreg,
+                                             int lane, const f32x16& sc0, const f32x16& sc1,
+                                             f32x16& sn0, f32x16& sn1, float& m, const PgenArgs& pa,
+                                             VOps<D>& vop) {
+  constexpr int KK = D / 16;
+  const uint8_t* p0 = kb_next + lane * 16;     // window 0 operand blocks
+  const uint8_t* p1 = p0 + KK * 1024;          // window 1 operand blocks
+  bf16x8 a0[2], a1[2];
+  PgenState st;
+  float pm0, pm1;
+
+  a0[0] = *(const bf16x8*)(p0);
+  a1[0] = *(const bf16x8*)(p1);
+  a0[1] = *(const bf16x8*)(p0 + 1024);
+  a1[1] = *(const bf16x8*)(p1 + 1024);
+  pg_max<KIND>(sc0, sc1, pm0, pm1);
+  __builtin_amdgcn_sched_barrier(0);
+
+  sn0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[0], qreg[0], f32x16{}, 0, 0, 0);
+  sn1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[0], qreg[0], f32x16{}, 0, 0, 0);
+  if constexpr (KK > 2) {
+    a0[0] = *(const bf16x8*)(p0 + 2 * 1024);
+    a1[0] = *(const bf16x8*)(p1 + 2 * 1024);
+  }
+  pg_params<KIND>(pm0, pm1, m, pa, st);
+  __builtin_amdgcn_sched_barrier(0);
+
+  qk_regions<D, KIND, 1>(p0, p1, a0, a1, qreg, sn0, sn1, vb, lane, vop, sc0, sc1, pa, st);
+  if constexpr (KIND == EFQ_PGEN_NOOP) asm volatile("" ::"v"(sc0), "v"(sc1));
+  return pg_finish<KIND>(st);
+}
+
+// Per-wave state of the fused kernel and one pipeline step.
+template <int D, int KIND, bool DUMP>
+struct WaveCtx {
+  static constexpr int NS = D / 32;   // 32-row slabs of O^T
+  bf16x8 qreg[D / 16];                // Q^T operand (lane: query my_q)
+  f32x16 oacc[NS];                    // O^T accumulators
+  f32x16 lacc;                        // row 0 carries l (P~ 1 on the MFMA)
+  float m;                            // running maximum
+  PgenArgs pa;
+  int lane, half, my_q, vis_end;
+
+  // Step j: the probability stage of tile j (scores c0, c1), the history
+  // rescale, and O^T += V~^T P~^T, l += P~ 1.  With NEXT, S(j+1) = K(j+1)
+  // Q^T is computed into n0, n1 in the same pass, interleaved region by
+  // region with the VALU work.
+  template <bool NEXT>
+  __device__ __forceinline__ void step(int j, const uint8_t* kbuf0, const uint8_t* vbuf0,
+                                       const AttnArgs& a, int b, int hq, const f32x16& c0,
+                                       const f32x16& c1, f32x16& n0, f32x16& n1) {
+    const uint8_t* vb = vbuf0 + (j % kStages) * Smem<D>::kV;
+    VOps<D> vop;
+    PgenOut po;
+    if constexpr (NEXT) {
+      po = step_next<D, KIND>(kbuf0 + ((j + 1) % kStages) * Smem<D>::kK, vb, qreg, lane, c0, c1,
+                              n0, n1, m, pa, vop);
+    } else {
+      read_v<D>(vb, lane, vop);
+      po = pgen<KIND>(c0, c1, m, pa);
+    }
+
+    if constexpr (DUMP) {
+      const int blk = 2 * j + half;
+      if (my_q < a.Sq && blk < a.nblk) {
+        long row = ((long)b * a.Hq + hq) * a.Sq + my_q;
+        *(u32x4*)(a.p_codes + (row * a.nblk + blk) * 16) = unpermute_codes(po.bop);
+        a.p_e8m0[row * a.nblk + blk] = (uint8_t)po.scale_b;
+      }
+    }
+
+    // ---- rescale history when a row maximum moved (alpha = 1 otherwise)
+    if (__builtin_amdgcn_ballot_w64(po.alpha != 1.0f) != 0ull) {
+#pragma unroll
+      for (int s = 0; s < NS; ++s) oacc[s] *= po.alpha;
+    }
+    lacc[0] *= po.alpha;
+
+    // ---- O^T += V~^T P~^T and l += P~ 1 on the FP4 MFMA (all-ones A, 2^0)
+    const i32x8 bop = i32x8{(int)po.bop[0], (int)po.bop[1], (int)po.bop[2], (int)po.bop[3], 0, 0, 0, 0};
+    pv_slabs<NS>(oacc, vop, bop, po.scale_b);
+    const i32x8 ones = i32x8{0x22222222, 0x22222222, 0x22222222, 0x22222222, 0, 0, 0, 0};
+    lacc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ones, bop, lacc, 4, 4, 0, 127, 0,
+                                                           po.scale_b);
+    if constexpr (NEXT) {
+      const int lim = vis_end - (j + 1) * kBc;
+      if (lim < kBc) mask_tile(n0, n1, lim, half);
+    }
+  }
+};
+
 template <int D, int KIND, bool CAUSAL, bool DUMP>
-__global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
+__global__ __launch_bounds__(kThreads, EFQ_WAVES_PER_SIMD) void attn_fwd_kernel(
     const unsigned short* __restrict__ q, const unsigned short* __restrict__ k,
     const uint8_t* __restrict__ vhat, float* __restrict__ out, AttnArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
-  constexpr int KK = D / 16;   // k-steps of the QK^T MFMA
+  constexpr int KK = D / 16;   // k-steps of the Q K^T MFMA
   constexpr int NS = D / 32;   // 32-row slabs of O^T
 
   int b, hq, qt;
   map_work(a, b, hq, qt);
   const int g = hq / (a.Hq / a.Hkv);
-  const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int half = lane >> 5;
+  WaveCtx<D, KIND, DUMP> w;
+  w.lane = threadIdx.x & 63;
+  w.half = w.lane >> 5;
   const int q_wave0 = qt * kBr + wave * kWaveQ;
-  const int my_q = q_wave0 + (lane & 31);
-  const int q_load = my_q < a.Sq ? my_q : a.Sq - 1;
+  w.my_q = q_wave0 + (w.lane & 31);
+  const int q_load = w.my_q < a.Sq ? w.my_q : a.Sq - 1;
 
   // Q^T operand in registers: lane holds Q[my_q][kk*16 + half*8 .. +8]
-  bf16x8 qreg[KK];
   {
-    const unsigned short* qp = q + (((long)b * a.Sq + q_load) * a.Hq + hq) * D + half * 8;
+    const unsigned short* qp = q + (((long)b * a.Sq + q_load) * a.Hq + hq) * D + w.half * 8;
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) qreg[kk] = *(const bf16x8*)(qp + kk * 16);
+    for (int kk = 0; kk < KK; ++kk) w.qreg[kk] = *(const bf16x8*)(qp + kk * 16);
   }
 
   const int kv_end = CAUSAL ? min(a.Sk, qt * kBr + kBr) : a.Sk;
   const int wave_end = CAUSAL ? min(a.Sk, q_wave0 + kWaveQ) : a.Sk;
-  const int ntiles = (kv_end + kBc - 1) / kBc;
+  const int ntiles = (kv_end + kBc - 1) / kBc;         // workgroup
+  const int wtiles = (wave_end + kBc - 1) / kBc;        // this wave
+  // visible keys of this lane: [0, vis_end)
+  w.vis_end = CAUSAL ? min(a.Sk, w.my_q + 1) : a.Sk;
 
-  const long kstride = (long)a.Hkv * D;
-  const unsigned short* kp = k + ((long)b * a.Sk * a.Hkv + g) * D;
-  const uint8_t* vcodes = vhat + ((long)b * a.Hkv + g) * a.nb * D * 16;
-  const uint8_t* vscales = vhat + a.scale_off + ((long)b * a.Hkv + g) * a.nb * D;
+  KLoad<D> kload;
+  kload.init(k + (long)b * a.Sk * a.Hkv * D, a.Sk, a.Hkv, g, wave, w.lane);
+  VLoad<D> vload;
+  vload.init(vhat + ((long)b * a.Hkv + g) * a.nb * D * 16,
+             vhat + a.scale_off + ((long)b * a.Hkv + g) * a.nb * D, a.nb);
+  uint8_t* const kbuf0 = smem + Smem<D>::kKOff;
+  uint8_t* const vbuf0 = smem + Smem<D>::kVOff;
+  const int v_issued = VLoad<D>::issued(wave);
 
-  PgenArgs pa;
-  pa.scale = a.scale;
-  pa.sh = a.scale * a.h;
-  pa.c = kLn6 + a.tau;
-  pa.negh = -a.h;
-  pa.l2s = a.scale * kInvLn2;
-
-  f32x16 oacc[NS];
+  w.pa.scale = a.scale;
+  w.pa.sh = a.scale * a.h;
+  w.pa.c = kLn6 + a.tau;
+  w.pa.negh = -a.h;
+  w.pa.l2s = a.scale * kInvLn2;
 #pragma unroll
-  for (int s = 0; s < NS; ++s) oacc[s] = f32x16{};
-  float m = -INFINITY;
-  float l = 0.0f;
-  const i32x8 ones = i32x8{0x22222222, 0x22222222, 0x22222222, 0x22222222, 0, 0, 0, 0};
+  for (int s = 0; s < NS; ++s) w.oacc[s] = f32x16{};
+  w.lacc = f32x16{};
+  w.m = -INFINITY;
 
-  TileRegs<D> tr;
-  load_tile<D>(tr, kp, vcodes, vscales, 0, a.Sk, kstride);
-  store_tile<D>(tr, smem);
+  // prologue: K(0) V~(0) K(1) | V~(1) K(2) in flight; S(0)
+  kload.issue(kbuf0, 0, wave);
+  vload.issue(vbuf0, 0, wave, w.lane);
+  int late = 0;
+  if (ntiles > 1) {
+    kload.issue(kbuf0 + Smem<D>::kK, 1, wave);
+    vload.issue(vbuf0 + Smem<D>::kV, 1, wave, w.lane);
+    late += v_issued;
+  }
+  if (ntiles > 2) {
+    kload.issue(kbuf0 + 2 * Smem<D>::kK, 2, wave);
+    late += KLoad<D>::kIssued;
+  }
+  wait_vmem_le(late);
+  __syncthreads();
+  f32x16 sa0, sa1, sb0, sb1;
+  if (wtiles > 0) {
+    qk_tile<D>(kbuf0, w.qreg, w.lane, sa0, sa1);
+    if (w.vis_end < kBc) mask_tile(sa0, sa1, w.vis_end, w.half);
+  }
 
-  for (int j = 0; j < ntiles; ++j) {
+  // One step: wait for the tile of the previous step's loads, publish it,
+  // stream K(j+3) and V~(j+2), compute.  Scores ping-pong between two
+  // register sets (two steps per loop trip) instead of being copied.
+  auto one = [&](int j, const f32x16& c0, const f32x16& c1, f32x16& n0, f32x16& n1) {
     __syncthreads();
-    const int key0 = j * kBc;
-    if (j + 1 < ntiles)
-      load_tile<D>(tr, kp, vcodes + (long)(j + 1) * 2 * D * 16, vscales + (long)(j + 1) * 2 * D,
-                   key0 + kBc, a.Sk, kstride);
-    const uint8_t* st = smem + (j & 1) * Smem<D>::kStage;
-
-    if (key0 < wave_end) {
-      // ---- S^T = K Q^T (bf16 MFMA), two 32-key windows
-      f32x16 s0 = f32x16{}, s1 = f32x16{};
-      const uint8_t* kr0 = st + (lane & 31) * Smem<D>::kRow + half * 16;
-      const uint8_t* kr1 = kr0 + 32 * Smem<D>::kRow;
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        bf16x8 a0 = *(const bf16x8*)(kr0 + kk * 32);
-        bf16x8 a1 = *(const bf16x8*)(kr1 + kk * 32);
-        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qreg[kk], s0, 0, 0, 0);
-        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qreg[kk], s1, 0, 0, 0);
-      }
-      // ---- mask (ragged key tail, causal diagonal), before P-gen
-      const bool need_mask = (key0 + kBc > a.Sk) || (CAUSAL && key0 + kBc - 1 > q_wave0);
-      if (need_mask) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          int kofs = 8 * (r >> 2) + 4 * half + (r & 3);
-          int t0 = key0 + kofs, t1 = key0 + 32 + kofs;
-          if (t0 >= a.Sk || (CAUSAL && t0 > my_q)) s0[r] = -INFINITY;
-          if (t1 >= a.Sk || (CAUSAL && t1 > my_q)) s1[r] = -INFINITY;
-        }
-      }
-      // ---- probability stage
-      PgenOut po = pgen<KIND>(s0, s1, m, pa);
-
-      if constexpr (DUMP) {
-        const int blk = 2 * j + half;
-        if (my_q < a.Sq && blk < a.nblk) {
-          long row = ((long)b * a.Hq + hq) * a.Sq + my_q;
-          *(u32x4*)(a.p_codes + (row * a.nblk + blk) * 16) = unpermute_codes(po.bop);
-          a.p_e8m0[row * a.nblk + blk] = (uint8_t)po.scale_b;
-        }
-      }
-
-      // ---- rescale history (skipped when no row maximum moved)
-      if (__builtin_amdgcn_ballot_w64(po.alpha != 1.0f) != 0ull) {
-#pragma unroll
-        for (int s = 0; s < NS; ++s) oacc[s] *= po.alpha;
-      }
-      l *= po.alpha;
-
-      // ---- O^T += V~^T P~^T on the FP4 MFMA; lane's A operand is the V~
-      // block (window `half`) of column s*32 + lane%32
-      const i32x8 bop = i32x8{(int)po.bop[0], (int)po.bop[1], (int)po.bop[2], (int)po.bop[3], 0, 0, 0, 0};
-      const uint8_t* vc = st + Smem<D>::kK + (half * D + (lane & 31)) * 16;
-      const uint8_t* vs = st + Smem<D>::kK + Smem<D>::kVc + half * D + (lane & 31);
-#pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        u32x4 av = *(const u32x4*)(vc + s * 32 * 16);
-        int sa = vs[s * 32];
-        i32x8 aop = i32x8{(int)av[0], (int)av[1], (int)av[2], (int)av[3], 0, 0, 0, 0};
-        oacc[s] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(aop, bop, oacc[s], 4, 4, 0, sa, 0,
-                                                                  po.scale_b);
-      }
-      // ---- denominator P~ 1 from the same operand (all-ones A, scale 2^0)
-      f32x16 lt = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ones, bop, f32x16{}, 4, 4, 0, 127,
-                                                                  0, po.scale_b);
-      l += lt[0];
+    int issued = 0;
+    if (j + 3 < ntiles) {
+      kload.issue(kbuf0 + (j % kStages) * Smem<D>::kK, j + 3, wave);
+      issued += KLoad<D>::kIssued;
     }
-
-    if (j + 1 < ntiles) store_tile<D>(tr, smem + ((j + 1) & 1) * Smem<D>::kStage);
+    if (j + 2 < ntiles) {
+      vload.issue(vbuf0 + ((j + 2) % kStages) * Smem<D>::kV, j + 2, wave, w.lane);
+      issued += v_issued;
+    }
+    if (j + 1 < wtiles)
+      w.template step<true>(j, kbuf0, vbuf0, a, b, hq, c0, c1, n0, n1);
+    else if (j < wtiles)
+      w.template step<false>(j, kbuf0, vbuf0, a, b, hq, c0, c1, n0, n1);
+    wait_vmem_le(issued);   // everything but this step's own loads has landed
+  };
+  for (int j = 0; j < ntiles; j += 2) {
+    one(j, sa0, sa1, sb0, sb1);
+    if (j + 1 < ntiles) one(j + 1, sb0, sb1, sa0, sa1);
   }
 
   // ---- O = A / l, fp32 store; lane holds query my_q, rows d of each slab
-  if (my_q < a.Sq) {
-    float* op = out + (((long)b * a.Sq + my_q) * a.Hq + hq) * D;
+  const float l = w.lacc[0];
+  if (w.my_q < a.Sq) {
+    float* op = out + (((long)b * a.Sq + w.my_q) * a.Hq + hq) * D;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {
-        int d = s * 32 + 8 * r4 + 4 * half;
-        f32x4 v4 = f32x4{oacc[s][4 * r4] / l, oacc[s][4 * r4 + 1] / l, oacc[s][4 * r4 + 2] / l,
-                         oacc[s][4 * r4 + 3] / l};
+        int d = s * 32 + 8 * r4 + 4 * w.half;
+        f32x4 v4 = f32x4{w.oacc[s][4 * r4] / l, w.oacc[s][4 * r4 + 1] / l,
+                         w.oacc[s][4 * r4 + 2] / l, w.oacc[s][4 * r4 + 3] / l};
         *(f32x4*)(op + d) = v4;
       }
     }
     if constexpr (DUMP) {
-      long row = ((long)b * a.Hq + hq) * a.Sq + my_q;
-      if (half == 0) {
-        a.row_m[row] = KIND == EFQ_PGEN_EXPQ ? m * kLn2 : m;
+      long row = ((long)b * a.Hq + hq) * a.Sq + w.my_q;
+      if (w.half == 0) {
+        a.row_m[row] = KIND == EFQ_PGEN_EXPQ ? w.m * kLn2 : w.m;
         a.row_l[row] = l;
       }
     }
@@ -731,6 +963,10 @@ int validate_shape(const efq_shape* s, int causal) {
     return fail(EFQ_EUNSUPPORTED, "grid too large");
   if ((long)s->seq_k > (1L << 30) || (long)s->seq_q > (1L << 30))
     return fail(EFQ_EUNSUPPORTED, "sequence too long");
+  // K of one batch and V~ of one (batch, kv head) are addressed through
+  // 32-bit buffer ranges
+  if ((long)s->seq_k * s->heads_kv * s->head_dim * 2 > 0x7FFFFFFFL)
+    return fail(EFQ_EUNSUPPORTED, "seq_k * heads_kv * head_dim * 2 must be below 2^31 bytes");
   return EFQ_OK;
 }
 
