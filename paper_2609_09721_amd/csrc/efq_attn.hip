@@ -51,6 +51,9 @@ constexpr int kWaves = 4;      // waves per workgroup
 constexpr int kBr = kWaveQ * kWaves;  // queries per workgroup
 constexpr int kBc = 64;        // keys per tile (two 32-key microscaling blocks)
 constexpr int kThreads = 64 * kWaves;
+#ifndef EFQ_PINGPONG
+#define EFQ_PINGPONG 1         // two wave groups in opposite MFMA / VALU phases
+#endif
 #ifndef EFQ_WAVES_PER_SIMD
 #define EFQ_WAVES_PER_SIMD 2   // fused-kernel occupancy target (register budget)
 #endif
@@ -423,10 +426,10 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, un
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
-template <int D>
+template <int D, int NW = kWaves>
 struct KLoad {
   static constexpr int KK = D / 16;
-  static constexpr int PER = 2 * KK / kWaves;            // 1 KB blocks per wave
+  static constexpr int PER = 2 * KK / NW;                // 1 KB blocks per wave
   static_assert(KK % PER == 0, "a wave's blocks share one 32-key window");
   const void* base;
   unsigned bytes;
@@ -453,7 +456,7 @@ struct KLoad {
   }
 };
 
-template <int D>
+template <int D, int NW = kWaves>
 struct VLoad {
   static constexpr int NB = Smem<D>::kVc / 1024;          // 1 KB code blocks (2 or 4)
   const uint8_t* codes;
@@ -465,14 +468,14 @@ struct VLoad {
     nb = nblocks;
   }
   // loads a wave issues per tile
-  __device__ static int issued(int wave) { return (wave < NB ? 1 : 0) + (wave == kWaves - 1 ? 1 : 0); }
+  __device__ static int issued(int wave) { return (wave < NB ? 1 : 0) + (wave == NW - 1 ? 1 : 0); }
   __device__ void issue(uint8_t* vbuf, int tile, int wave, int lane) const {
     const auto rc = make_rsrc(codes, (unsigned)(nb * D * 16));
     const auto rs = make_rsrc(scales, (unsigned)(nb * D));
     if (wave < NB)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, vbuf + wave * 1024, 16, lane * 16,
                                                tile * 2 * D * 16 + wave * 1024, 0, 0);
-    if (wave == kWaves - 1) {
+    if (wave == NW - 1) {
       // 2 D scale bytes as dwords; for D = 64 the upper lanes repeat the
       // lower ones into the padding
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, vbuf + Smem<D>::kVc, 4, (lane % (2 * D / 4)) * 4,
@@ -572,11 +575,23 @@ __device__ __forceinline__ void pv_slabs(f32x16* oacc, const VOps<D>& v, const i
 // (the mask acts before the probability stage).  lim = number of visible
 // keys of this lane counted from the tile start.
 __device__ __forceinline__ void mask_tile(f32x16& s0, f32x16& s1, int lim, int half) {
+  const int l0 = lim - 4 * half;   // the per-register key offsets stay immediates
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
-    const int kofs = 8 * (r >> 2) + 4 * half + (r & 3);
-    s0[r] = kofs < lim ? s0[r] : -INFINITY;
-    s1[r] = kofs + 32 < lim ? s1[r] : -INFINITY;
+    const int kofs = 8 * (r >> 2) + (r & 3);
+    s0[r] = kofs < l0 ? s0[r] : -INFINITY;
+    s1[r] = kofs + 32 < l0 ? s1[r] : -INFINITY;
+  }
+}
+
+// History rescale A *= alpha, l *= alpha, skipped (a uniform branch) on
+// tiles where no row maximum of the wave moved (alpha = 1 on all lanes).
+template <int NS>
+__device__ __forceinline__ void rescale(f32x16* oacc, f32x16& lacc, float alpha) {
+  if (__builtin_amdgcn_ballot_w64(alpha != 1.0f) != 0ull) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s) oacc[s] *= alpha;
+    lacc[0] *= alpha;
   }
 }
 
@@ -683,11 +698,7 @@ struct WaveCtx {
     }
 
     // ---- rescale history when a row maximum moved (alpha = 1 otherwise)
-    if (__builtin_amdgcn_ballot_w64(po.alpha != 1.0f) != 0ull) {
-#pragma unroll
-      for (int s = 0; s < NS; ++s) oacc[s] *= po.alpha;
-    }
-    lacc[0] *= po.alpha;
+    rescale<NS>(oacc, lacc, po.alpha);
 
     // ---- O^T += V~^T P~^T and l += P~ 1 on the FP4 MFMA (all-ones A, 2^0)
     const i32x8 bop = i32x8{(int)po.bop[0], (int)po.bop[1], (int)po.bop[2], (int)po.bop[3], 0, 0, 0, 0};
@@ -824,6 +835,300 @@ __global__ __launch_bounds__(kThreads, EFQ_WAVES_PER_SIMD) void attn_fwd_kernel(
   }
 }
 
+// ------------------------------------------------- ping-pong variant
+// Eight waves per workgroup (two per SIMD, 256 queries) in two groups of
+// four.  Each tile is split into a matrix-core phase M(j) = P~V of tile j-1
+// and S(j) = K(j) Q^T, and a VALU phase V(j) = the probability stage of
+// tile j and the history rescale.  The groups run opposite phases between
+// workgroup barriers, so on every SIMD one wave feeds the matrix core while
+// the other runs the probability stage:
+//   phase 2j:    group 0 runs M(j),  group 1 runs V(j-1)
+//   phase 2j+1:  group 0 runs V(j),  group 1 runs M(j)
+// K(j) is read in phases 2j and 2j+1, V~(j) in phases 2j+2 and 2j+3.  Both
+// stream through three-stage rings, issued at an even phase four phases
+// before their first use and waited for at the end of the next phase.
+constexpr int kPPWaves = 8;
+constexpr int kPPBr = kWaveQ * kPPWaves;   // queries per workgroup
+constexpr int kPPThreads = 64 * kPPWaves;
+
+// P~1 on the 16x16x128 FP4 MFMA.  Its B operand is the P~^T operand of the
+// P~V product as it sits in the lanes (lane l: query l % 32, key block
+// l / 32), read as a 128 x 16 matrix (lane l: column l % 16, K block l / 16).
+// The A operand `sel` is 1.0 in row 4h of K block g when g and h have the
+// same parity, 0 elsewhere; then row 4 (l / 16) of column l % 16, which lane
+// l holds in element 0 of the result, is the sum over both key blocks of
+// lane l's own query.  The other rows stay 0.
+__device__ __forceinline__ i32x8 rowsum_selector(int lane) {
+  const int m = lane & 15, g = lane >> 4;
+  const int v = ((m & 3) == 0 && (g & 1) == ((m >> 2) & 1)) ? 0x22222222 : 0;
+  return i32x8{v, v, v, v, 0, 0, 0, 0};
+}
+
+__device__ __forceinline__ f32x4 rowsum_mfma(const i32x8& sel, const i32x8& b8, const f32x4& l, int sb) {
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(sel, b8, l, 4, 4, 0, 127, 0, sb);
+}
+
+// S = K Q^T of one 64-key tile with the LDS operand reads kept PD k-steps
+// ahead of the MFMAs; with PV, the P~V and P~1 MFMAs of the previous tile
+// (operands already in registers) run first, under the latency of the first
+// K reads.  sched_group_barrier fixes that order.
+template <int D, bool PV>
+__device__ __forceinline__ void mma_phase(const uint8_t* kbuf, const bf16x8* qreg, int lane,
+                                          f32x16& s0, f32x16& s1, f32x16* oacc, f32x4& lacc,
+                                          const i32x8& sel, const VOps<D>& vop, const u32x4& bop,
+                                          int sb) {
+  constexpr int KK = D / 16;
+  constexpr int NS = D / 32;
+  constexpr int PD = KK < 3 ? KK : 3;
+  const uint8_t* p0 = kbuf + lane * 16;
+  const uint8_t* p1 = p0 + KK * 1024;
+  bf16x8 a0[KK], a1[KK];
+#pragma unroll
+  for (int kk = 0; kk < PD; ++kk) {
+    a0[kk] = *(const bf16x8*)(p0 + kk * 1024);
+    a1[kk] = *(const bf16x8*)(p1 + kk * 1024);
+  }
+  if constexpr (PV) {
+    const i32x8 b8 = i32x8{(int)bop[0], (int)bop[1], (int)bop[2], (int)bop[3], 0, 0, 0, 0};
+    pv_slabs<NS>(oacc, vop, b8, sb);
+    lacc = rowsum_mfma(sel, b8, lacc, sb);
+  }
+  s0 = f32x16{};
+  s1 = f32x16{};
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[kk], qreg[kk], s0, 0, 0, 0);
+    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[kk], qreg[kk], s1, 0, 0, 0);
+    if (kk + PD < KK) {
+      a0[kk + PD] = *(const bf16x8*)(p0 + (kk + PD) * 1024);
+      a1[kk + PD] = *(const bf16x8*)(p1 + (kk + PD) * 1024);
+    }
+  }
+  // order: first K reads | P~V, P~1 MFMAs | per k-step: 2 MFMAs, 2 K reads
+  __builtin_amdgcn_sched_group_barrier(0x100, 2 * PD, 0);
+  if constexpr (PV) __builtin_amdgcn_sched_group_barrier(0x008, NS + 1, 0);
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    if (kk + PD < KK) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  }
+}
+
+template <int D, int KIND, bool DUMP>
+struct PPWave {
+  static constexpr int NS = D / 32;
+  bf16x8 qreg[D / 16];
+  f32x16 oacc[NS];
+  f32x4 lacc;             // element 0: the lane's row sum l
+  i32x8 sel;              // A operand of the P~1 MFMA
+  float m;
+  PgenArgs pa;
+  int lane, half, my_q, vis_end;
+
+  // M(j): P~V of tile j-1 (with PV), then S(j) = K(j) Q^T.
+  template <bool PV>
+  __device__ __forceinline__ void mma(int j, const uint8_t* kbuf0, const VOps<D>& vop,
+                                      const u32x4& bop, int sb, f32x16& s0, f32x16& s1) {
+    mma_phase<D, PV>(kbuf0 + (j % kStages) * Smem<D>::kK, qreg, lane, s0, s1, oacc, lacc, sel,
+                     vop, bop, sb);
+  }
+
+  __device__ __forceinline__ void pv(const VOps<D>& vop, const u32x4& bop, int sb) {
+    const i32x8 b8 = i32x8{(int)bop[0], (int)bop[1], (int)bop[2], (int)bop[3], 0, 0, 0, 0};
+    pv_slabs<NS>(oacc, vop, b8, sb);
+    lacc = rowsum_mfma(sel, b8, lacc, sb);
+  }
+
+  // V(j): read the V~(j) operands for the next matrix phase, mask the
+  // scores of tile j (diagonal and ragged tiles only), run the probability
+  // stage into (bop, sb), and rescale the history.
+  __device__ __forceinline__ void vphase(int j, const AttnArgs& a, int b, int hq,
+                                         const uint8_t* vbuf0, f32x16& s0, f32x16& s1,
+                                         VOps<D>& vop, u32x4& bop, int& sb) {
+    read_v<D>(vbuf0 + (j % kStages) * Smem<D>::kV, lane, vop);
+    const int lim = vis_end - j * kBc;
+    if (__builtin_amdgcn_ballot_w64(lim < kBc) != 0ull) mask_tile(s0, s1, lim, half);
+    PgenOut po = pgen<KIND>(s0, s1, m, pa);
+    bop = po.bop;
+    sb = po.scale_b;
+    if constexpr (DUMP) {
+      const int blk = 2 * j + half;
+      if (my_q < a.Sq && blk < a.nblk) {
+        long row = ((long)b * a.Hq + hq) * a.Sq + my_q;
+        *(u32x4*)(a.p_codes + (row * a.nblk + blk) * 16) = unpermute_codes(po.bop);
+        a.p_e8m0[row * a.nblk + blk] = (uint8_t)po.scale_b;
+      }
+    }
+    if (__builtin_amdgcn_ballot_w64(po.alpha != 1.0f) != 0ull) {
+#pragma unroll
+      for (int s = 0; s < NS; ++s) oacc[s] *= po.alpha;
+      lacc[0] *= po.alpha;
+    }
+  }
+};
+
+template <int D, int KIND, bool CAUSAL, bool DUMP>
+__global__ __attribute__((amdgpu_flat_work_group_size(kPPThreads, kPPThreads),
+                          amdgpu_waves_per_eu(2, 2))) void
+attn_pp_kernel(const unsigned short* __restrict__ q, const unsigned short* __restrict__ k,
+               const uint8_t* __restrict__ vhat, float* __restrict__ out, AttnArgs a) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  constexpr int KK = D / 16;
+  constexpr int NS = D / 32;
+
+  int b, hq, qt;
+  map_work(a, b, hq, qt);
+  const int g = hq / (a.Hq / a.Hkv);
+  // wave index as a uniform (scalar) value: the group branch below is uniform
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int group = wave >> 2;
+  PPWave<D, KIND, DUMP> w;
+  w.lane = threadIdx.x & 63;
+  w.half = w.lane >> 5;
+  const int q_wave0 = qt * kPPBr + wave * kWaveQ;
+  w.my_q = q_wave0 + (w.lane & 31);
+  const int q_load = w.my_q < a.Sq ? w.my_q : a.Sq - 1;
+  {
+    const unsigned short* qp = q + (((long)b * a.Sq + q_load) * a.Hq + hq) * D + w.half * 8;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) w.qreg[kk] = *(const bf16x8*)(qp + kk * 16);
+  }
+  // tiles of the workgroup and of this wave (1 <= wtiles <= ntiles)
+  const int kv_end = CAUSAL ? min(a.Sk, qt * kPPBr + kPPBr) : a.Sk;
+  const int wave_end = CAUSAL ? min(a.Sk, q_wave0 + kWaveQ) : a.Sk;
+  const int ntiles = (kv_end + kBc - 1) / kBc;
+  const int wtiles = (wave_end + kBc - 1) / kBc;
+  w.vis_end = CAUSAL ? min(a.Sk, w.my_q + 1) : a.Sk;
+
+  KLoad<D, kPPWaves> kload;
+  kload.init(k + (long)b * a.Sk * a.Hkv * D, a.Sk, a.Hkv, g, wave, w.lane);
+  VLoad<D, kPPWaves> vload;
+  vload.init(vhat + ((long)b * a.Hkv + g) * a.nb * D * 16,
+             vhat + a.scale_off + ((long)b * a.Hkv + g) * a.nb * D, a.nb);
+  uint8_t* const kbuf0 = smem + Smem<D>::kKOff;
+  uint8_t* const vbuf0 = smem + Smem<D>::kVOff;
+  const int v_issued = VLoad<D, kPPWaves>::issued(wave);
+
+  w.pa.scale = a.scale;
+  w.pa.sh = a.scale * a.h;
+  w.pa.c = kLn6 + a.tau;
+  w.pa.negh = -a.h;
+  w.pa.l2s = a.scale * kInvLn2;
+#pragma unroll
+  for (int s = 0; s < NS; ++s) w.oacc[s] = f32x16{};
+  w.lacc = f32x4{0.f, 0.f, 0.f, 0.f};
+  w.sel = rowsum_selector(w.lane);
+  w.m = -INFINITY;
+
+  // prologue: K(0), K(1), V~(0) resident; K(2), V~(1) in flight
+  kload.issue(kbuf0, 0, wave);
+  if (ntiles > 1) kload.issue(kbuf0 + Smem<D>::kK, 1, wave);
+  vload.issue(vbuf0, 0, wave, w.lane);
+  int batch = 0;
+  if (ntiles > 2) {
+    kload.issue(kbuf0 + 2 * Smem<D>::kK, 2, wave);
+    batch += KLoad<D, kPPWaves>::kIssued;
+  }
+  if (ntiles > 1) {
+    vload.issue(vbuf0 + Smem<D>::kV, 1, wave, w.lane);
+    batch += v_issued;
+  }
+  wait_vmem_le(batch);
+  __syncthreads();
+
+  // Trip j >= 1 streams K(j+2) (replacing K(j-1)) and V~(j+1) (replacing
+  // V~(j-2)); returns the number of loads issued.
+  auto stream = [&](int j) {
+    int n = 0;
+    if (j + 2 < ntiles) {
+      kload.issue(kbuf0 + ((j + 2) % kStages) * Smem<D>::kK, j + 2, wave);
+      n += KLoad<D, kPPWaves>::kIssued;
+    }
+    if (j + 1 < ntiles) {
+      vload.issue(vbuf0 + ((j + 1) % kStages) * Smem<D>::kV, j + 1, wave, w.lane);
+      n += v_issued;
+    }
+    return n;
+  };
+
+  // Every wave passes two barriers per trip j = 0 .. ntiles.  The wave's own
+  // tiles run in trips 0 .. wtiles (the first without P~V, the last with
+  // P~V only); later trips only keep the loads and barriers in step.
+  f32x16 s0, s1;
+  VOps<D> vop;
+  u32x4 bop;
+  int sb;
+  // Each loop body ends with a matrix phase, whose results feed the next
+  // trip: this keeps its MFMAs on their side of the barrier.
+  if (group == 0) {
+    w.template mma<false>(0, kbuf0, vop, bop, 0, s0, s1);   // phase 0
+    __syncthreads();
+    for (int j = 1; j < wtiles; ++j) {
+      w.vphase(j - 1, a, b, hq, vbuf0, s0, s1, vop, bop, sb);   // phase 2j-1
+      wait_vmem_le(batch);
+      __syncthreads();
+      batch = stream(j);                                       // phase 2j
+      w.template mma<true>(j, kbuf0, vop, bop, sb, s0, s1);
+      __syncthreads();
+    }
+    w.vphase(wtiles - 1, a, b, hq, vbuf0, s0, s1, vop, bop, sb);
+    wait_vmem_le(batch);
+    __syncthreads();
+    batch = stream(wtiles);
+    w.pv(vop, bop, sb);
+    __syncthreads();
+    wait_vmem_le(batch);
+    __syncthreads();
+  } else {
+    __syncthreads();
+    w.template mma<false>(0, kbuf0, vop, bop, 0, s0, s1);
+    wait_vmem_le(batch);
+    __syncthreads();
+    for (int j = 1; j < wtiles; ++j) {
+      batch = stream(j);
+      w.vphase(j - 1, a, b, hq, vbuf0, s0, s1, vop, bop, sb);
+      __syncthreads();
+      w.template mma<true>(j, kbuf0, vop, bop, sb, s0, s1);
+      wait_vmem_le(batch);
+      __syncthreads();
+    }
+    batch = stream(wtiles);
+    w.vphase(wtiles - 1, a, b, hq, vbuf0, s0, s1, vop, bop, sb);
+    __syncthreads();
+    w.pv(vop, bop, sb);
+    wait_vmem_le(batch);
+    __syncthreads();
+  }
+  for (int j = wtiles + 1; j <= ntiles; ++j) {
+    batch = stream(j);
+    __syncthreads();
+    wait_vmem_le(batch);
+    __syncthreads();
+  }
+
+  const float l = w.lacc[0];
+  if (w.my_q < a.Sq) {
+    float* op = out + (((long)b * a.Sq + w.my_q) * a.Hq + hq) * D;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        int d = s * 32 + 8 * r4 + 4 * w.half;
+        f32x4 v4 = f32x4{w.oacc[s][4 * r4] / l, w.oacc[s][4 * r4 + 1] / l,
+                         w.oacc[s][4 * r4 + 2] / l, w.oacc[s][4 * r4 + 3] / l};
+        *(f32x4*)(op + d) = v4;
+      }
+    }
+    if constexpr (DUMP) {
+      long row = ((long)b * a.Hq + hq) * a.Sq + w.my_q;
+      if (w.half == 0) {
+        a.row_m[row] = KIND == EFQ_PGEN_EXPQ ? w.m * kLn2 : w.m;
+        a.row_l[row] = l;
+      }
+    }
+  }
+}
+
 // ------------------------------------------ standalone probability stage
 // One wave per (32 rows, 64 columns) tile of x: the values are placed into
 // the accumulator layout of the fused kernel and run through the same code
@@ -912,6 +1217,12 @@ __global__ void fill_zero_kernel(uint8_t* __restrict__ p, size_t n) {
 }
 
 // ================================================================ host side
+#if EFQ_PINGPONG
+constexpr int kQTile = kPPBr;   // queries per workgroup of the launched kernel
+#else
+constexpr int kQTile = kBr;
+#endif
+
 thread_local char g_msg[512] = "ok";
 
 int fail(int status, const char* fmt, ...) {
@@ -958,7 +1269,7 @@ int validate_shape(const efq_shape* s, int causal) {
   if (causal && s->seq_q != s->seq_k)
     return fail(EFQ_EUNSUPPORTED, "causal attention needs seq_q == seq_k (%d != %d)", s->seq_q,
                 s->seq_k);
-  const long nqt = (s->seq_q + kBr - 1) / kBr;
+  const long nqt = (s->seq_q + kQTile - 1) / kQTile;
   if ((long)s->batch * s->heads_q * nqt > 0x7FFFFFFFL)
     return fail(EFQ_EUNSUPPORTED, "grid too large");
   if ((long)s->seq_k > (1L << 30) || (long)s->seq_q > (1L << 30))
@@ -1001,9 +1312,15 @@ int launch_vquant(const void* v, const efq_shape* s, void* vhat, hipStream_t st)
 template <int D, int KIND, bool CAUSAL, bool DUMP>
 hipError_t launch_attn_t(const void* q, const void* k, const void* vhat, float* out,
                          const AttnArgs& a, hipStream_t st, unsigned grid) {
+#if EFQ_PINGPONG
+  hipLaunchKernelGGL((attn_pp_kernel<D, KIND, CAUSAL, DUMP>), dim3(grid), dim3(kPPThreads),
+                     Smem<D>::kTotal, st, (const unsigned short*)q, (const unsigned short*)k,
+                     (const uint8_t*)vhat, out, a);
+#else
   hipLaunchKernelGGL((attn_fwd_kernel<D, KIND, CAUSAL, DUMP>), dim3(grid), dim3(kThreads),
                      Smem<D>::kTotal, st, (const unsigned short*)q, (const unsigned short*)k,
                      (const uint8_t*)vhat, out, a);
+#endif
   return hipGetLastError();
 }
 
@@ -1041,7 +1358,7 @@ int launch_attn(const void* q, const void* k, const void* vhat, float scale, int
   a.Hkv = s->heads_kv;
   a.nb = (int)padded_blocks(s->seq_k);
   a.scale_off = vhat_scale_offset(s);
-  a.nqt = (s->seq_q + kBr - 1) / kBr;
+  a.nqt = (s->seq_q + kQTile - 1) / kQTile;
   a.scale = scale;
   a.tau = p.tau;
   a.h = p.h;
