@@ -35,15 +35,21 @@
  *   M_b  = max_{t in b} x_t                         Alg. 1, block maximum
  *   k_b  = floor(fl(fl(M_b + log(2/9)) * (1/log2))) Eq. (k-rule), k_b >= -127
  *   off  = fl(fl(k_b * log2) + fl(log6 + tau))      k_b log2 + log6 + tau
- *   u_t  = fma(acc_t, fl(scale*h), -fl(fl(m + off) * h))
- *        ~ (x_t - k_b log2 - log6 - tau) h = (z_t - tau) h    Eq. (d8-index)
- *   c_t  = clip(floor(u_t) + 1, 0, 7)
+ *   B    = -fl(fl(m + off) * h)
+ *   EFQ:  w_t = fma(acc_t, 32 fl(scale*h), fl(32 B + 31.5))
+ *             ~ 32 (u_t + 1) - 1/2,  u_t = (x_t - k_b log2 - log6 - tau) h
+ *                                        = (z_t - tau) h      Eq. (d8-index)
+ *         c_t = floor(min(max(rne(w_t), 0), 255) / 32)
+ *   LUT:  u_t = fma(acc_t, fl(scale*h), B),  j16 = clip(floor(u_t) + 1, 0, 15)
  *
- * The residual argument (z_t - tau) h is one fused multiply-add of the raw
- * dot product with the row and block terms folded into a bias; in exact
- * arithmetic it is the paper's expression, in fp32 it can differ from a
- * step-by-step evaluation only within a few ulps of a code threshold.
- * orc_pgen_real evaluates the same steps in fp64 to pin that.
+ * In exact arithmetic floor(min(max(rne(32 v - 1/2), 0), 255) / 32) is
+ * clip(floor(v), 0, 7) for every real v (a half-integer 32 n - 1/2 rounds
+ * to the even 32 n, and 32 n + 31.5 only occurs at v = n + 1), so c_t is
+ * clip(floor(u_t) + 1, 0, 7) of Eq. (d8-index).  The residual argument is
+ * one fused multiply-add of the raw dot product with the row and block
+ * terms folded into a bias; in fp32 it can differ from a step-by-step
+ * evaluation only within a few ulps of a code threshold.  orc_pgen_real
+ * evaluates the same steps in fp64 to pin that.
  *
  * Build: gcc -O2 -std=gnu99 -ffp-contract=off -fno-fast-math -fopenmp
  *        -shared -fPIC efq_oracle.c -lm
@@ -82,6 +88,18 @@ static float bf16_to_f32(uint16_t b)
 }
 
 static int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
+
+/* E2M1 code from w ~ 32 (u + 1) - 1/2: round to nearest (ties to even),
+ * saturate to [0, 255], keep the multiple of 32.  -inf and NaN give 0. */
+static int code_from_w(float w)
+{
+    float r = nearbyintf(w); /* default rounding: nearest, ties to even */
+    if (!(r > 0.0f))
+        return 0;
+    if (r > 255.0f)
+        r = 255.0f;
+    return (int)r / 32;
+}
 
 /* floor(u) + 1 clipped to [0, top]; u = -inf or below gives 0. */
 static int affine_index(float u, int top)
@@ -158,7 +176,9 @@ static int pgen_block(const float *acc, int n, float scale, float m, float tau,
     /* Alg. 1: z_t = x_t - k_b log2 - log6 (Eq. z-def), then
      * c_t = clip(floor((z_t - tau) h) + 1, 0, 7) (Eq. d8-index), or for the
      * LUT variant j16 = clip(floor((z_t - tau16) h16) + 1, 0, 15), c_t = C16[j16].
-     * (z_t - tau) h is evaluated as acc_t (scale h) - (m + k_b log2 + log6 + tau) h. */
+     * (z_t - tau) h is evaluated as acc_t (scale h) - (m + k_b log2 + log6 + tau) h;
+     * for EFQ the floor, the +1 and both clips come from rounding
+     * 32 ((z_t - tau) h + 1) - 1/2 to an integer in [0, 255] (header). */
     float kf = (float)k;
     float klog2 = kf * F_LN2;
     float c0 = F_LN6 + tau;
@@ -166,16 +186,20 @@ static int pgen_block(const float *acc, int n, float scale, float m, float tau,
     float moff = m + off;
     float bias = -(moff * h);
     float sh = scale * h;
+    float sh32 = 32.0f * sh;                  /* exact */
+    float bias32 = fmaf(bias, 32.0f, 31.5f);  /* fl(32 B + 31.5) */
     for (int t = 0; t < n; ++t) {
         if (acc[t] == -INFINITY) {
             codes[t] = 0;
             continue;
         }
-        float u = fmaf(acc[t], sh, bias);
-        if (lut)
+        if (lut) {
+            float u = fmaf(acc[t], sh, bias);
             codes[t] = (uint8_t)C16[affine_index(u, 15)];
-        else
-            codes[t] = (uint8_t)affine_index(u, 7);
+        } else {
+            float w = fmaf(acc[t], sh32, bias32);
+            codes[t] = (uint8_t)code_from_w(w);
+        }
     }
     return k;
 }

@@ -69,13 +69,19 @@ def pgen_fp32(x: np.ndarray, tau: float, h: float, lut: bool = False,
     k = np.where(fin, k, -127)
     off = (k.astype(F32) * LN2) + (LN6 + tau)
     bias = -((m + off) * h)
-    u = fma32(np.where(masked, F32(0), xp), F32(scale * h), bias[:, :, None])
-    fu = np.floor(u.astype(np.float64))
+    acc = np.where(masked, F32(0), xp)
     if lut:
+        u = fma32(acc, F32(scale * h), bias[:, :, None])
+        fu = np.floor(u.astype(np.float64))
         j = np.clip(fu + 1, 0, 15).astype(np.int64)
         c = C16[j]
     else:
-        c = np.clip(fu + 1, 0, 7).astype(np.int64)
+        # w ~ 32 (u + 1) - 1/2; nearest-even to an integer, saturate to
+        # [0, 255], keep the multiple of 32: clip(floor(u) + 1, 0, 7)
+        bias32 = fma32(bias, F32(32.0), F32(31.5))
+        w = fma32(acc, F32(32.0) * F32(scale * h), bias32[:, :, None])
+        r = np.rint(w.astype(np.float64))
+        c = (np.clip(r, 0, 255) // 32).astype(np.int64)
     c = np.where(masked, 0, c)
     return c.reshape(rows, nblk * 32)[:, :cols], k
 
