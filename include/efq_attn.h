@@ -102,7 +102,7 @@ enum efq_status {
  * The scales start at byte offset efq_vhat_scale_offset(s).  Within the 16
  * code bytes the 32 keys are stored in the order the FP4 matrix core reads
  * them: key t of the block sits in nibble e(t) = 8*(2*((t>>2)&1) + (t>>4))
- * + 4*((t>>3)&1) + (t&3) (byte e/2, low nibble for even e).
+ * + 2*(t&3) + ((t>>3)&1) (byte e/2, low nibble for even e).
  * ------------------------------------------------------------------------- */
 size_t efq_vhat_bytes(const efq_shape *s);
 size_t efq_vhat_scale_offset(const efq_shape *s);

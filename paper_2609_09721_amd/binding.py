@@ -257,7 +257,7 @@ def vhat_natural(vhat: torch.Tensor, shape: Shape):
     codes = vhat[: B * H * nb * D * 16].view(B, H, nb, D, 16)
     nib = unpack_nibbles(codes)                        # [B, H, nb, D, 32] nibble order
     t = torch.arange(32)
-    e = (8 * (2 * ((t >> 2) & 1) + (t >> 4)) + 4 * ((t >> 3) & 1) + (t & 3)).to(vhat.device)
+    e = (8 * (2 * ((t >> 2) & 1) + (t >> 4)) + 2 * (t & 3) + ((t >> 3) & 1)).to(vhat.device)
     keyed = nib[..., e]                                # [..., 32] key order
     codes_nat = keyed.permute(0, 1, 2, 4, 3).reshape(B, H, nb * 32, D)
     # scale plane: byte (d % 32) * (D / 32) + d / 32 of each block

@@ -92,16 +92,22 @@ __device__ __forceinline__ float max16(const f32x16& v) {
   return m;
 }
 
+// Operand dword dw of a lane holds the codes of accumulator elements
+// j = 0..7 of one window and half-lane: element j sits in nibble
+// 2 (j % 4) + j / 4 (the byte-then-nibble assembly of the probability stage).
+__host__ __device__ __forceinline__ constexpr int elem_nibble(int j) { return 2 * (j & 3) + (j >> 2); }
+
 // Key offset (0..31) of nibble e of the 16-byte FP4 operand of a lane.
 __host__ __device__ __forceinline__ int nibble_key(int e) {
   int dw = e >> 3, nib = e & 7;
-  int r = ((dw & 1) << 3) + nib;   // accumulator index of the producing lane
-  int gq = dw >> 1;                // which half-lane produced it
+  int j = 4 * (nib & 1) + (nib >> 1);   // element within the dword
+  int r = ((dw & 1) << 3) + j;          // accumulator index of the producing lane
+  int gq = dw >> 1;                     // which half-lane produced it
   return 8 * (r >> 2) + 4 * gq + (r & 3);
 }
 // Inverse: nibble position of key t (0..31).
 __host__ __device__ __forceinline__ int key_nibble(int t) {
-  return 8 * (2 * ((t >> 2) & 1) + (t >> 4)) + 4 * ((t >> 3) & 1) + (t & 3);
+  return 8 * (2 * ((t >> 2) & 1) + (t >> 4)) + 2 * (t & 3) + ((t >> 3) & 1);
 }
 
 // -------------------------------------------------- probability stage
@@ -122,6 +128,7 @@ __host__ __device__ __forceinline__ int key_nibble(int t) {
 struct PgenArgs {
   float scale;   // softmax scale
   float sh;      // fl(scale * h)
+  float sh32;    // 32 fl(scale * h)   (EFQ code argument, exact)
   float c;       // fl(log 6 + tau)
   float negh;    // -h
   float l2s;     // fl(scale * log2 e)   (exp-then-quantize)
@@ -134,7 +141,9 @@ struct PgenOut {
 };
 
 struct PgenState {
-  float bias[2];      // EFQ/LUT: -(m + k_b log2 + log6 + tau) h per window
+  float bias[2];      // per window: LUT B = -(m + k_b log2 + log6 + tau) h,
+                      // EFQ fl(32 B + 31.5)
+  unsigned d[2];      // EFQ: byte-packed codes of the current dword
   float sc[2];        // EXPQ: 2^k_b per window (fp32 scale of the conversion)
   float mq;           // EXPQ: running maximum in log2 units
   int scale_b;        // E8M0 of the lane's own block
@@ -204,47 +213,72 @@ __device__ __forceinline__ void pg_params(float pm0, float pm1, float& m, const 
       // (z_t - tau) h with z_t = x_t - k_b log2 - log6 (Eq. z-def), folded to
       // fma(acc, scale h, bias), bias = -(m + k_b log2 + log6 + tau) h
       const float off = (float)kb * kLn2 + pa.c;
-      float b0 = (m + off) * pa.negh, b1 = b0;
+      float b0 = (m + off) * pa.negh;
+      // EFQ: w_t = fma(acc_t, 32 scale h, fl(32 B + 31.5)) ~ 32 (u_t + 1) - 1/2
+      if constexpr (KIND == EFQ_PGEN_EFQ) b0 = __builtin_fmaf(b0, 32.0f, 31.5f);
+      float b1 = b0;
       swap32f(b0, b1);                          // (bias of block 0, bias of block 1)
       st.bias[0] = b0;
       st.bias[1] = b1;
       st.scale_b = kb + 127;
-      // packed codes start at 0x11111111: each element adds (c - 1) << 4e
+      // LUT: packed codes start at 0x11111111, each element adds (c - 1)
       st.w[0] = st.w[1] = st.w[2] = st.w[3] = 0x11111111u;
     }
   }
 }
 
-// Code minus one of one score: u = (z_t - tau) h, Eq. (d8-index), and
-// c - 1 = clip(floor(u), -1, 6); for EFQ-Softmax-LUT the 16-level index
-// j16 = clip(floor(u) + 1, 0, 15) folded through C16 (Sec. II-D).
-template <int KIND>
-__device__ __forceinline__ int pg_code_m1(float acc, const PgenArgs& pa, float bias) {
+// EFQ-Softmax-LUT, Sec. II-D: the 16-level index j16 = clip(floor(u) + 1,
+// 0, 15) of u = (z_t - tau16) h16, folded through C16; returns the code
+// minus one.
+__device__ __forceinline__ int pg_lut_code_m1(float acc, const PgenArgs& pa, float bias) {
   const float u = __builtin_fmaf(acc, pa.sh, bias);
-  const int f = cvt_flr(u);
-  if constexpr (KIND == EFQ_PGEN_LUT) {
-    const int j = clampi(f, -1, 14) + 1;
-    return (int)((kC16 >> (4 * j)) & 0xF) - 1;
-  } else {
-    return clampi(f, -1, 6);
-  }
+  const int j = clampi(cvt_flr(u), -1, 14) + 1;
+  return (int)((kC16 >> (4 * j)) & 0xF) - 1;
 }
 
-// Codes of elements E and E+1 (same window, same dword).
+// EFQ code of one score into byte BYTE of d: c = clip(floor(u) + 1, 0, 7)
+// of Eq. (d8-index) is bits 7..5 of sat[0,255](rne(w)), w ~ 32 (u + 1) - 1/2
+// (a half-integer 32 n - 1/2 rounds to the even 32 n; w < 0 saturates to
+// code 0, u + 1 >= 8 to 255, code 7).  One conversion per score.
+template <int BYTE>
+__device__ __forceinline__ unsigned pg_efq_byte(float acc, const PgenArgs& pa, float bias32,
+                                                unsigned d) {
+  const float w = __builtin_fmaf(acc, pa.sh32, bias32);
+  return __builtin_amdgcn_cvt_pk_u8_f32(w, BYTE, BYTE == 0 ? 0u : d);
+}
+
+// Codes of elements E and E+1 (same window, same dword DW = E / 8).  In
+// dword DW, element j = E % 8 sits in nibble elem_nibble(j).
 template <int KIND, int E>
 __device__ __forceinline__ void pg_pair(const f32x16& s0, const f32x16& s1, const PgenArgs& pa,
                                         PgenState& st) {
   if constexpr (KIND != EFQ_PGEN_NOOP) {
-    constexpr int WIN = E / 16, R = E % 16, DW = E / 8, NIB = E % 8;
+    constexpr int WIN = E / 16, R = E % 16, DW = E / 8, J = E % 8;
     const f32x16& s = WIN ? s1 : s0;
     if constexpr (KIND == EFQ_PGEN_EXPQ) {
-      const float p0 = __builtin_amdgcn_exp2f(s[R] * pa.l2s - st.mq);
-      const float p1 = __builtin_amdgcn_exp2f(s[R + 1] * pa.l2s - st.mq);
-      // RNE(p / 2^k) to E2M1 with saturation, two codes into byte NIB/2
-      st.w[DW] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(st.w[DW], p0, p1, st.sc[WIN], NIB / 2);
+      // RNE(p / 2^k) to E2M1 with saturation; elements j and j + 4 share
+      // byte j, so the pair is converted once both are known
+      if constexpr (J < 4) {
+        const float p0 = __builtin_amdgcn_exp2f(s[R] * pa.l2s - st.mq);
+        const float p1 = __builtin_amdgcn_exp2f(s[R + 4] * pa.l2s - st.mq);
+        st.w[DW] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(st.w[DW], p0, p1, st.sc[WIN], J);
+        const float p2 = __builtin_amdgcn_exp2f(s[R + 1] * pa.l2s - st.mq);
+        const float p3 = __builtin_amdgcn_exp2f(s[R + 5] * pa.l2s - st.mq);
+        st.w[DW] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(st.w[DW], p2, p3, st.sc[WIN], J + 1);
+      }
+    } else if constexpr (KIND == EFQ_PGEN_LUT) {
+      st.w[DW] = lshl_add_imm<4 * elem_nibble(J)>(pg_lut_code_m1(s[R], pa, st.bias[WIN]), st.w[DW]);
+      st.w[DW] = lshl_add_imm<4 * elem_nibble(J + 1)>(pg_lut_code_m1(s[R + 1], pa, st.bias[WIN]),
+                                                      st.w[DW]);
     } else {
-      st.w[DW] = lshl_add_imm<4 * NIB>(pg_code_m1<KIND>(s[R], pa, st.bias[WIN]), st.w[DW]);
-      st.w[DW] = lshl_add_imm<4 * NIB + 4>(pg_code_m1<KIND>(s[R + 1], pa, st.bias[WIN]), st.w[DW]);
+      // elements 0..3 of the dword into the bytes of d[0], 4..7 into d[1]
+      unsigned& d = st.d[J >> 2];
+      d = pg_efq_byte<J & 3>(s[R], pa, st.bias[WIN], d);
+      d = pg_efq_byte<(J & 3) + 1>(s[R + 1], pa, st.bias[WIN], d);
+      if constexpr (J == 6) {
+        // nibble 2b <- bits 7..5 of byte b of d[0], nibble 2b+1 <- of d[1]
+        st.w[DW] = ((st.d[0] >> 5) & 0x07070707u) | ((st.d[1] >> 1) & 0x70707070u);
+      }
     }
   }
 }
@@ -757,6 +791,7 @@ __global__ __launch_bounds__(kThreads, EFQ_WAVES_PER_SIMD) void attn_fwd_kernel(
 
   w.pa.scale = a.scale;
   w.pa.sh = a.scale * a.h;
+  w.pa.sh32 = 32.0f * w.pa.sh;
   w.pa.c = kLn6 + a.tau;
   w.pa.negh = -a.h;
   w.pa.l2s = a.scale * kInvLn2;
@@ -1011,6 +1046,7 @@ attn_pp_kernel(const unsigned short* __restrict__ q, const unsigned short* __res
 
   w.pa.scale = a.scale;
   w.pa.sh = a.scale * a.h;
+  w.pa.sh32 = 32.0f * w.pa.sh;
   w.pa.c = kLn6 + a.tau;
   w.pa.negh = -a.h;
   w.pa.l2s = a.scale * kInvLn2;
@@ -1158,6 +1194,7 @@ __global__ __launch_bounds__(64) void pgen_kernel(const float* __restrict__ x,
   PgenArgs pa;
   pa.scale = 1.0f;
   pa.sh = 1.0f * a.h;
+  pa.sh32 = 32.0f * pa.sh;
   pa.c = kLn6 + a.tau;
   pa.negh = -a.h;
   pa.l2s = 1.0f * kInvLn2;
@@ -1195,6 +1232,7 @@ __global__ __launch_bounds__(256) void pgen_bench_kernel(int iters, float tau, f
   PgenArgs pa;
   pa.scale = 0.0883883461f;
   pa.sh = pa.scale * h;
+  pa.sh32 = 32.0f * pa.sh;
   pa.c = kLn6 + tau;
   pa.negh = -h;
   pa.l2s = pa.scale * kInvLn2;
