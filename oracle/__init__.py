@@ -65,7 +65,7 @@ def lib():
         L.orc_quant_v.argtypes = [P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, P, P]
         L.orc_attn.argtypes = [P, P, P] + [ctypes.c_int] * 6 + [
             ctypes.c_float, ctypes.c_int, ctypes.c_int, ctypes.c_float, ctypes.c_float,
-            ctypes.c_int, P, ctypes.c_long, P, P, P, P, P, ctypes.c_int]
+            ctypes.c_int, P, ctypes.c_long, P, P, P, P, P, P, ctypes.c_int]
         for f in (L.orc_pgen, L.orc_pgen_real, L.orc_quant_v, L.orc_attn):
             f.restype = ctypes.c_int
         _lib = L
@@ -139,13 +139,14 @@ def all_rows(B: int, Hq: int, Sq: int) -> np.ndarray:
 
 def attn(q_bits, k_bits, v_bits, scale: float, causal: bool, mode: int = EFQ,
          tau: float = None, h: float = None, bc: int = 64, rows: np.ndarray = None,
-         dump: bool = False, nthreads: int = 0):
+         dump: bool = False, nthreads: int = 0, margins: bool = False):
     """Attention forward for the listed query rows (Alg. 2 over tiles of bc keys).
 
     q_bits [B, Sq, Hq, D], k_bits/v_bits [B, Sk, Hkv, D]: bf16 bit patterns.
     rows: int32 [n, 3] of (b, hq, i); None = every row, ordered (b, hq, i).
     Returns out [n, D] fp32, plus (codes [n, nblk*32], e8m0 [n, nblk],
-    m [n] fp32, l [n] fp64) when dump is set."""
+    m [n] fp32, l [n] fp64) when dump is set, plus the per-row smallest
+    decision margin [n] fp64 (in dot-product units) when margins is set."""
     q_bits = np.ascontiguousarray(q_bits, dtype=np.uint16)
     k_bits = np.ascontiguousarray(k_bits, dtype=np.uint16)
     v_bits = np.ascontiguousarray(v_bits, dtype=np.uint16)
@@ -164,14 +165,19 @@ def attn(q_bits, k_bits, v_bits, scale: float, causal: bool, mode: int = EFQ,
         e8 = np.zeros((n, nblk), np.uint8)
         mm = np.zeros((n,), np.float32)
         ll = np.zeros((n,), np.float64)
+    mg = np.full((n,), np.inf, np.float64) if margins else None
     rc = lib().orc_attn(_ptr(q_bits), _ptr(k_bits), _ptr(v_bits), B, Sq, Sk, Hq, Hkv, D,
                         float(scale), int(causal), int(mode), tau, h, int(bc), _ptr(rows), n,
-                        _ptr(out), _ptr(codes), _ptr(e8), _ptr(mm), _ptr(ll), int(nthreads))
+                        _ptr(out), _ptr(codes), _ptr(e8), _ptr(mm), _ptr(ll), _ptr(mg),
+                        int(nthreads))
     if rc != 0:
         raise ValueError(f"orc_attn failed with {rc}")
+    res = (out,)
     if dump:
-        return out, codes, e8, mm, ll
-    return out
+        res += (codes, e8, mm, ll)
+    if margins:
+        res += (mg,)
+    return res if len(res) > 1 else out
 
 
 def bf16_bits(t) -> np.ndarray:

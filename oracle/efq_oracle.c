@@ -146,9 +146,17 @@ static int floor_log2(double a)
  * by the attention mask, Sec. III-D: masks act before P-gen), together with
  * the softmax scale and the running row maximum m, so x_t = fl(S_t - m).
  * Writes codes[t] in 0..7 and returns k_b.
+ *
+ * Diagnostic (margin != NULL): lowers *margin to the smallest distance, in
+ * units of the raw dot product, between an argument of this block's
+ * decisions and the nearest value where that decision changes (k_b at
+ * integer q, an EFQ code at w = 32 n - 1/2, a LUT index at integer u).  It
+ * does not change any result; a check that compares against an
+ * implementation whose dot products differ in the last bits uses it to
+ * tell a legitimate code flip from an error.
  * ---------------------------------------------------------------------- */
 static int pgen_block(const float *acc, int n, float scale, float m, float tau,
-                      float h, int lut, uint8_t *codes)
+                      float h, int lut, uint8_t *codes, double *margin)
 {
     /* Alg. 1: M_b = max_t x_t (masked keys do not take part). */
     float Mb = -INFINITY;
@@ -171,6 +179,12 @@ static int pgen_block(const float *acc, int n, float scale, float m, float tau,
         float q = a * F_INVLN2;
         float fq = floorf(q);
         k = fq < (float)K_MIN ? K_MIN : (fq > (float)K_MAX ? K_MAX : (int)fq);
+        if (margin && q > (float)K_MIN - 0.5f) {
+            double dq = fabs((double)q - nearbyint((double)q));
+            double d = dq / ((double)F_INVLN2 * (double)scale);
+            if (d < *margin)
+                *margin = d;
+        }
     }
 
     /* Alg. 1: z_t = x_t - k_b log2 - log6 (Eq. z-def), then
@@ -196,9 +210,23 @@ static int pgen_block(const float *acc, int n, float scale, float m, float tau,
         if (lut) {
             float u = fmaf(acc[t], sh, bias);
             codes[t] = (uint8_t)C16[affine_index(u, 15)];
+            if (margin) {
+                double nb = nearbyint((double)u);
+                nb = nb < 0.0 ? 0.0 : (nb > 14.0 ? 14.0 : nb);
+                double d = fabs((double)u - nb) / (double)sh;
+                if (d < *margin)
+                    *margin = d;
+            }
         } else {
             float w = fmaf(acc[t], sh32, bias32);
             codes[t] = (uint8_t)code_from_w(w);
+            if (margin) {
+                double nb = nearbyint(((double)w + 0.5) / 32.0);
+                nb = nb < 1.0 ? 1.0 : (nb > 7.0 ? 7.0 : nb);
+                double d = fabs((double)w - (32.0 * nb - 0.5)) / (double)sh32;
+                if (d < *margin)
+                    *margin = d;
+            }
         }
     }
     return k;
@@ -253,7 +281,7 @@ int orc_pgen(const float *x, long rows, int cols, int mode, float tau, float h,
             if (mode == ORC_EXPQ)
                 k = pgen_block_expq(xb, n, 1.0f, 0.0f, cb);
             else
-                k = pgen_block(xb, n, 1.0f, 0.0f, tau, h, mode == ORC_LUT, cb);
+                k = pgen_block(xb, n, 1.0f, 0.0f, tau, h, mode == ORC_LUT, cb, NULL);
             e8m0[r * nblk + b] = (uint8_t)(k + 127);
         }
     }
@@ -371,13 +399,15 @@ static double e2m1_value(uint8_t c, int k)
  * exp-then-quantize path, V as MXFP4.  ORC_EXACT: fp64 softmax with
  * unquantised V (the unquantised reference of the calibration objective).
  * Optional dumps (may be NULL): codes [nrows][nblk*32] (one code per byte),
- * e8m0 [nrows][nblk], final m (fp32, score units) and l (fp64) per row.
+ * e8m0 [nrows][nblk], final m (fp32, score units) and l (fp64) per row,
+ * and row_margin [nrows]: the smallest decision margin of the row (EFQ and
+ * LUT; see pgen_block), +inf when no decision was taken.
  * ---------------------------------------------------------------------- */
 int orc_attn(const uint16_t *q, const uint16_t *kmat, const uint16_t *v, int B, int Sq,
              int Sk, int Hq, int Hkv, int D, float scale, int causal, int mode, float tau,
              float h, int bc, const int32_t *rows, long nrows, float *out,
              uint8_t *dump_codes, uint8_t *dump_e8m0, float *dump_m, double *dump_l,
-             int nthreads)
+             double *row_margin, int nthreads)
 {
     if (!q || !kmat || !v || !rows || !out || B < 1 || Sq < 1 || Sk < 1 || Hq < 1 ||
         Hkv < 1 || D < 1 || Hq % Hkv != 0 || bc < 32 || bc % 32 != 0 || bc > 1024)
@@ -447,6 +477,7 @@ int orc_attn(const uint16_t *q, const uint16_t *kmat, const uint16_t *v, int B, 
         if (dump_e8m0)
             memset(dump_e8m0 + r * (long)nblk, 0, (size_t)nblk);
         const int kend = causal ? i + 1 : Sk; /* keys [0, kend) are visible */
+        double margin = INFINITY;             /* diagnostic, see pgen_block */
         float m = -INFINITY;                  /* running max, score units */
         double mx = -INFINITY;                /* running max, fp64 (EXACT) */
         double l = 0.0;
@@ -519,7 +550,7 @@ int orc_attn(const uint16_t *q, const uint16_t *kmat, const uint16_t *v, int B, 
                     kb = pgen_block_expq(acc + b0, 32, scale, mnew, cd + b0);
                 else
                     kb = pgen_block(acc + b0, 32, scale, mnew, tau, h, mode == ORC_LUT,
-                                    cd + b0);
+                                    cd + b0, row_margin ? &margin : NULL);
                 int blk = (j0 + b0) / 32;
                 if (blk < nblk) {
                     if (dump_e8m0)
@@ -550,6 +581,8 @@ int orc_attn(const uint16_t *q, const uint16_t *kmat, const uint16_t *v, int B, 
             dump_m[r] = (mode == ORC_EXACT) ? (float)mx : m;
         if (dump_l)
             dump_l[r] = l;
+        if (row_margin)
+            row_margin[r] = margin;
         free(acc); free(cd); free(A); free(dA); free(qd);
     }
     free(vhat);
@@ -557,4 +590,4 @@ int orc_attn(const uint16_t *q, const uint16_t *kmat, const uint16_t *v, int B, 
 }
 
 /* Version tag so the Python side can tell a stale build. */
-int orc_version(void) { return 1; }
+int orc_version(void) { return 2; }

@@ -381,6 +381,25 @@ def test_single_visible_key(orc):
     assert np.array_equal(out[0], vhat.astype(np.float32))
 
 
+def test_decision_margin_single_key(orc):
+    """Causal row 0: the only visible score is the row maximum, so M_b = 0
+    and k_b = floor(log(2/9) / log 2) = -3 (Eq. k-rule).  The nearest
+    decision change is that floor at the integer -2, at a distance
+    |2 log 2 + log(2/9)| / scale in dot-product units; the code of the max
+    (u ~ 7.70 for Mean, code 7) is farther from its thresholds."""
+    w, q, k, v = _tiny(S=96, causal=True, Hq=1, Hkv=1)
+    rows = np.array([[0, 0, 0]], np.int32)
+    out, mg = orc.attn(orc.bf16_bits(q), orc.bf16_bits(k), orc.bf16_bits(v), w.scale, True,
+                       orc.EFQ, rows=rows, margins=True)
+    want = abs(2 * math.log(2) + math.log(2 / 9)) / w.scale
+    assert abs(mg[0] - want) <= 1e-5 * want
+    # more keys can only bring a decision closer to its threshold
+    rows = np.array([[0, 0, i] for i in range(96)], np.int32)
+    _, mg = orc.attn(orc.bf16_bits(q), orc.bf16_bits(k), orc.bf16_bits(v), w.scale, True,
+                     orc.EFQ, rows=rows, margins=True)
+    assert np.all(mg > 0) and np.all(mg <= want * (1 + 1e-5))
+
+
 def _dominant_key0(D=64, S=256, seed=3):
     """Dyadic inputs where key 0 holds the maximum score of every row."""
     g = torch.Generator().manual_seed(seed)
