@@ -519,6 +519,21 @@ struct VLoad {
 };
 
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Workgroup barrier without the release fence of __syncthreads, which would
+// wait for every outstanding global->LDS load (vmcnt(0)) at each barrier,
+// although a tile is needed only several phases after its load is issued.
+// The loads' consumers wait on vmcnt explicitly (wait_vmem_le) before the
+// barrier that publishes them.  LDS reads need no wait here: every ring
+// slot is read, and the read consumed, at least one barrier before the next
+// load into it is issued.  The "memory" clobber keeps the compiler from
+// moving LDS accesses across the barrier, the scheduling barriers keep the
+// matrix-core and VALU work of a phase on its side.
+__device__ __forceinline__ void wg_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_barrier" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
 // Wait until at most n vector-memory loads of this wave are outstanding
 // (loads complete in issue order); n is wave-uniform and at most 6.
 __device__ __forceinline__ void wait_vmem_le(int n) {
@@ -1098,49 +1113,50 @@ attn_pp_kernel(const unsigned short* __restrict__ q, const unsigned short* __res
   // trip: this keeps its MFMAs on their side of the barrier.
   if (group == 0) {
     w.template mma<false>(0, kbuf0, vop, bop, 0, s0, s1);   // phase 0
-    __syncthreads();
+    wg_barrier();
     for (int j = 1; j < wtiles; ++j) {
       w.vphase(j - 1, a, b, hq, vbuf0, s0, s1, vop, bop, sb);   // phase 2j-1
       wait_vmem_le(batch);
-      __syncthreads();
+      wg_barrier();
       batch = stream(j);                                       // phase 2j
       w.template mma<true>(j, kbuf0, vop, bop, sb, s0, s1);
-      __syncthreads();
+      wg_barrier();
     }
     w.vphase(wtiles - 1, a, b, hq, vbuf0, s0, s1, vop, bop, sb);
     wait_vmem_le(batch);
-    __syncthreads();
+    wg_barrier();
     batch = stream(wtiles);
     w.pv(vop, bop, sb);
-    __syncthreads();
+    wg_barrier();
     wait_vmem_le(batch);
-    __syncthreads();
+    wg_barrier();
   } else {
-    __syncthreads();
+    wg_barrier();
     w.template mma<false>(0, kbuf0, vop, bop, 0, s0, s1);
     wait_vmem_le(batch);
-    __syncthreads();
+    wg_barrier();
     for (int j = 1; j < wtiles; ++j) {
       batch = stream(j);
       w.vphase(j - 1, a, b, hq, vbuf0, s0, s1, vop, bop, sb);
-      __syncthreads();
+      wg_barrier();
       w.template mma<true>(j, kbuf0, vop, bop, sb, s0, s1);
       wait_vmem_le(batch);
-      __syncthreads();
+      wg_barrier();
     }
     batch = stream(wtiles);
     w.vphase(wtiles - 1, a, b, hq, vbuf0, s0, s1, vop, bop, sb);
-    __syncthreads();
+    wg_barrier();
     w.pv(vop, bop, sb);
     wait_vmem_le(batch);
-    __syncthreads();
+    wg_barrier();
   }
   for (int j = wtiles + 1; j <= ntiles; ++j) {
     batch = stream(j);
-    __syncthreads();
+    wg_barrier();
     wait_vmem_le(batch);
-    __syncthreads();
+    wg_barrier();
   }
+  wait_vmem();   // no load may still target LDS when the wave leaves
 
   const float l = w.lacc[0];
   if (w.my_q < a.Sq) {
