@@ -438,7 +438,8 @@ struct AttnArgs {
 // K and V~ have three buffers each: step j reads K of tile j+1 and V~ of
 // tile j while K of tile j+3 and V~ of tile j+2 stream in, so a load has
 // two steps to land.
-constexpr int kStages = 3;
+constexpr int kStages = 3;    // K ring depth
+constexpr int kVStages = 4;   // V~ ring depth (the ping-pong kernel streams V~ one tile earlier)
 template <int D>
 struct Smem {
   static constexpr int kK = kBc * D * 2;                 // one K tile
@@ -447,7 +448,7 @@ struct Smem {
   static constexpr int kV = kVc + kVs;                   // one V~ tile
   static constexpr int kKOff = 0;
   static constexpr int kVOff = kStages * kK;
-  static constexpr int kTotal = kStages * (kK + kV);
+  static constexpr int kTotal = kStages * kK + kVStages * kV;
 };
 
 // Direct-to-LDS loads (buffer_load ... lds: LDS address = M0 base + size *
@@ -918,50 +919,65 @@ __device__ __forceinline__ f32x4 rowsum_mfma(const i32x8& sel, const i32x8& b8, 
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(sel, b8, l, 4, 4, 0, 127, 0, sb);
 }
 
-// S = K Q^T of one 64-key tile with the LDS operand reads kept PD k-steps
-// ahead of the MFMAs; with PV, the P~V and P~1 MFMAs of the previous tile
-// (operands already in registers) run first, under the latency of the first
-// K reads.  sched_group_barrier fixes that order.
-template <int D, bool PV>
-__device__ __forceinline__ void mma_phase(const uint8_t* kbuf, const bf16x8* qreg, int lane,
-                                          f32x16& s0, f32x16& s1, f32x16* oacc, f32x4& lacc,
-                                          const i32x8& sel, const VOps<D>& vop, const u32x4& bop,
-                                          int sb) {
+// Matrix phase of the ping-pong kernel.  With QK: S = K Q^T of one 64-key
+// tile into (sn0, sn1), the LDS operand reads kept PD k-steps ahead.  With
+// CODES: the per-score part of the probability stage of the previous tile
+// (scores sc0, sc1, block parameters in st) runs on the VALU in the shadow
+// of those MFMAs, one slice per k-step region (sched_barrier keeps the
+// regions in order), then its P~V and P~1 MFMAs close the phase.
+template <int D, int KIND, bool QK, int I>
+__device__ __forceinline__ void mc_regions(const uint8_t* p0, const uint8_t* p1, bf16x8* a0,
+                                           bf16x8* a1, const bf16x8* qreg, f32x16& sn0,
+                                           f32x16& sn1, const f32x16& sc0, const f32x16& sc1,
+                                           const PgenArgs& pa, PgenState& st) {
   constexpr int KK = D / 16;
-  constexpr int NS = D / 32;
+  constexpr int PD = KK < 3 ? KK : 3;
+  if constexpr (I < KK) {
+    if constexpr (QK) {
+      sn0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[I], qreg[I], sn0, 0, 0, 0);
+      sn1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[I], qreg[I], sn1, 0, 0, 0);
+      if constexpr (I + PD < KK) {
+        a0[I + PD] = *(const bf16x8*)(p0 + (I + PD) * 1024);
+        a1[I + PD] = *(const bf16x8*)(p1 + (I + PD) * 1024);
+      }
+    }
+    constexpr int P0 = 16 * I / KK, P1 = 16 * (I + 1) / KK;
+    pg_pairs<KIND, 2 * P0, 2 * P1>(sc0, sc1, pa, st);
+    __builtin_amdgcn_sched_barrier(0);
+    mc_regions<D, KIND, QK, I + 1>(p0, p1, a0, a1, qreg, sn0, sn1, sc0, sc1, pa, st);
+  }
+}
+
+template <int D, int KIND, bool QK, bool CODES>
+__device__ __forceinline__ PgenOut mma_phase(const uint8_t* kbuf, const bf16x8* qreg, int lane,
+                                             f32x16& sn0, f32x16& sn1, const f32x16& sc0,
+                                             const f32x16& sc1, const PgenArgs& pa,
+                                             PgenState& st) {
+  constexpr int KK = D / 16;
   constexpr int PD = KK < 3 ? KK : 3;
   const uint8_t* p0 = kbuf + lane * 16;
   const uint8_t* p1 = p0 + KK * 1024;
   bf16x8 a0[KK], a1[KK];
+  if constexpr (QK) {
 #pragma unroll
-  for (int kk = 0; kk < PD; ++kk) {
-    a0[kk] = *(const bf16x8*)(p0 + kk * 1024);
-    a1[kk] = *(const bf16x8*)(p1 + kk * 1024);
-  }
-  if constexpr (PV) {
-    const i32x8 b8 = i32x8{(int)bop[0], (int)bop[1], (int)bop[2], (int)bop[3], 0, 0, 0, 0};
-    pv_slabs<NS>(oacc, vop, b8, sb);
-    lacc = rowsum_mfma(sel, b8, lacc, sb);
-  }
-  s0 = f32x16{};
-  s1 = f32x16{};
-#pragma unroll
-  for (int kk = 0; kk < KK; ++kk) {
-    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[kk], qreg[kk], s0, 0, 0, 0);
-    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[kk], qreg[kk], s1, 0, 0, 0);
-    if (kk + PD < KK) {
-      a0[kk + PD] = *(const bf16x8*)(p0 + (kk + PD) * 1024);
-      a1[kk + PD] = *(const bf16x8*)(p1 + (kk + PD) * 1024);
+    for (int kk = 0; kk < PD; ++kk) {
+      a0[kk] = *(const bf16x8*)(p0 + kk * 1024);
+      a1[kk] = *(const bf16x8*)(p1 + kk * 1024);
     }
+    sn0 = f32x16{};
+    sn1 = f32x16{};
   }
-  // order: first K reads | P~V, P~1 MFMAs | per k-step: 2 MFMAs, 2 K reads
-  __builtin_amdgcn_sched_group_barrier(0x100, 2 * PD, 0);
-  if constexpr (PV) __builtin_amdgcn_sched_group_barrier(0x008, NS + 1, 0);
-#pragma unroll
-  for (int kk = 0; kk < KK; ++kk) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-    if (kk + PD < KK) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  __builtin_amdgcn_sched_barrier(0);
+  PgenOut po{};
+  if constexpr (CODES) {
+    mc_regions<D, KIND, QK, 0>(p0, p1, a0, a1, qreg, sn0, sn1, sc0, sc1, pa, st);
+    if constexpr (KIND == EFQ_PGEN_NOOP) asm volatile("" ::"v"(sc0), "v"(sc1));   // keep Q K^T live
+    po = pg_finish<KIND>(st);
+  } else {
+    f32x16 z{};
+    mc_regions<D, EFQ_PGEN_NOOP, QK, 0>(p0, p1, a0, a1, qreg, sn0, sn1, z, z, pa, st);
   }
+  return po;
 }
 
 template <int D, int KIND, bool DUMP>
@@ -973,49 +989,100 @@ struct PPWave {
   i32x8 sel;              // A operand of the P~1 MFMA
   float m;
   PgenArgs pa;
+  PgenState st;           // block parameters of the tile between V(j) and M(j+1)
   int lane, half, my_q, vis_end;
 
-  // M(j): P~V of tile j-1 (with PV), then S(j) = K(j) Q^T.
-  template <bool PV>
-  __device__ __forceinline__ void mma(int j, const uint8_t* kbuf0, const VOps<D>& vop,
-                                      const u32x4& bop, int sb, f32x16& s0, f32x16& s1) {
-    mma_phase<D, PV>(kbuf0 + (j % kStages) * Smem<D>::kK, qreg, lane, s0, s1, oacc, lacc, sel,
-                     vop, bop, sb);
+  // Matrix phase M(j): with CODES the codes of tile j-1 (scores sc) and its
+  // P~V, P~1; with QK the scores of tile j into sn.
+  template <bool QK, bool CODES>
+  __device__ __forceinline__ void mphase(int j, const uint8_t* kbuf0, const VOps<D>& vop,
+                                         const AttnArgs& a, int b, int hq, f32x16& sn0,
+                                         f32x16& sn1, const f32x16& sc0, const f32x16& sc1) {
+    const uint8_t* kb = kbuf0 + ((QK ? j : 0) % kStages) * Smem<D>::kK;
+    PgenOut po = mma_phase<D, KIND, QK, CODES>(kb, qreg, lane, sn0, sn1, sc0, sc1, pa, st);
+    if constexpr (CODES) {
+      if constexpr (DUMP) {
+        const int blk = 2 * (j - 1) + half;
+        if (my_q < a.Sq && blk < a.nblk) {
+          long row = ((long)b * a.Hq + hq) * a.Sq + my_q;
+          *(u32x4*)(a.p_codes + (row * a.nblk + blk) * 16) = unpermute_codes(po.bop);
+          a.p_e8m0[row * a.nblk + blk] = (uint8_t)po.scale_b;
+        }
+      }
+      const i32x8 b8 = i32x8{(int)po.bop[0], (int)po.bop[1], (int)po.bop[2], (int)po.bop[3], 0, 0, 0, 0};
+      pv_slabs<NS>(oacc, vop, b8, po.scale_b);
+      lacc = rowsum_mfma(sel, b8, lacc, po.scale_b);
+    }
   }
 
-  __device__ __forceinline__ void pv(const VOps<D>& vop, const u32x4& bop, int sb) {
-    const i32x8 b8 = i32x8{(int)bop[0], (int)bop[1], (int)bop[2], (int)bop[3], 0, 0, 0, 0};
-    pv_slabs<NS>(oacc, vop, b8, sb);
-    lacc = rowsum_mfma(sel, b8, lacc, sb);
-  }
-
-  // V(j): read the V~(j) operands for the next matrix phase, mask the
-  // scores of tile j (diagonal and ragged tiles only), run the probability
-  // stage into (bop, sb), and rescale the history.
-  __device__ __forceinline__ void vphase(int j, const AttnArgs& a, int b, int hq,
-                                         const uint8_t* vbuf0, f32x16& s0, f32x16& s1,
-                                         VOps<D>& vop, u32x4& bop, int& sb) {
-    read_v<D>(vbuf0 + (j % kStages) * Smem<D>::kV, lane, vop);
+  // VALU phase V(j): read the V~(j) operands for the next matrix phase, mask
+  // the scores of tile j (diagonal and ragged tiles only), take the block
+  // and row maxima and the block parameters (row maximum, alpha, k_b, bias),
+  // and rescale the history when a row maximum moved.
+  __device__ __forceinline__ void vphase(int j, const uint8_t* vbuf0, f32x16& s0, f32x16& s1,
+                                         VOps<D>& vop) {
+    read_v<D>(vbuf0 + (j % kVStages) * Smem<D>::kV, lane, vop);
     const int lim = vis_end - j * kBc;
     if (__builtin_amdgcn_ballot_w64(lim < kBc) != 0ull) mask_tile(s0, s1, lim, half);
-    PgenOut po = pgen<KIND>(s0, s1, m, pa);
-    bop = po.bop;
-    sb = po.scale_b;
-    if constexpr (DUMP) {
-      const int blk = 2 * j + half;
-      if (my_q < a.Sq && blk < a.nblk) {
-        long row = ((long)b * a.Hq + hq) * a.Sq + my_q;
-        *(u32x4*)(a.p_codes + (row * a.nblk + blk) * 16) = unpermute_codes(po.bop);
-        a.p_e8m0[row * a.nblk + blk] = (uint8_t)po.scale_b;
-      }
-    }
-    if (__builtin_amdgcn_ballot_w64(po.alpha != 1.0f) != 0ull) {
+    float pm0, pm1;
+    pg_max<KIND>(s0, s1, pm0, pm1);
+    pg_params<KIND>(pm0, pm1, m, pa, st);
+    if (__builtin_amdgcn_ballot_w64(st.alpha != 1.0f) != 0ull) {
 #pragma unroll
-      for (int s = 0; s < NS; ++s) oacc[s] *= po.alpha;
-      lacc[0] *= po.alpha;
+      for (int s = 0; s < NS; ++s) oacc[s] *= st.alpha;
+      lacc[0] *= st.alpha;
     }
   }
 };
+
+// The per-wave schedule of the ping-pong kernel.  A wave with T tiles runs
+// M(0) V(0) M(1) V(1) ... M(T-1) V(T-1) F, where M(j) also codes tile j-1
+// and applies its P~V (j >= 1) and F codes and applies the last tile; group
+// G runs op o in phase o + G, so K(j) is read in phases 2j, 2j+1 and V~(j)
+// in phases 2j+1, 2j+2.  Phase t ends with a barrier; even phases t = 2j
+// >= 2 start by streaming K(j+2) and V~(j+2), odd phases end by waiting
+// until only the loads of the even phase before are outstanding (loads
+// complete in order).  A load issued in phase 2j has therefore landed by
+// the end of phase 2j+3, in time for K(j+2) in phase 2j+4 and V~(j+2) in
+// phase 2j+5; the slots it overwrites (K(j-1), V~(j-2)) were last read,
+// and the reads consumed, by phase 2j-1.  Every wave passes 2 ntiles + 2
+// barriers.  Scores alternate between two register sets.
+template <int G, int D, int KIND, bool DUMP, typename Stream>
+__device__ __forceinline__ void pp_schedule(PPWave<D, KIND, DUMP>& w, int T, int ntiles,
+                                            const uint8_t* kbuf0, const uint8_t* vbuf0,
+                                            const AttnArgs& a, int b, int hq, int batch,
+                                            Stream stream) {
+  f32x16 sa0, sa1, sb0, sb1;
+  VOps<D> vop;
+  int t = 0;   // phase
+  auto begin = [&]() {
+    if ((t & 1) == 0 && t >= 2) batch = stream(t >> 1);
+  };
+  auto end = [&]() {
+    if (t & 1) wait_vmem_le(batch);
+    wg_barrier();
+    ++t;
+  };
+  if (G == 1) { begin(); end(); }
+  // M(0), V(0)
+  begin(); w.template mphase<true, false>(0, kbuf0, vop, a, b, hq, sa0, sa1, sb0, sb1); end();
+  begin(); w.vphase(0, vbuf0, sa0, sa1, vop); end();
+  int j = 1;
+  for (; j + 1 < T; j += 2) {
+    begin(); w.template mphase<true, true>(j, kbuf0, vop, a, b, hq, sb0, sb1, sa0, sa1); end();
+    begin(); w.vphase(j, vbuf0, sb0, sb1, vop); end();
+    begin(); w.template mphase<true, true>(j + 1, kbuf0, vop, a, b, hq, sa0, sa1, sb0, sb1); end();
+    begin(); w.vphase(j + 1, vbuf0, sa0, sa1, vop); end();
+  }
+  if (j < T) {   // one more tile: its scores go to set b, the last coded from b
+    begin(); w.template mphase<true, true>(j, kbuf0, vop, a, b, hq, sb0, sb1, sa0, sa1); end();
+    begin(); w.vphase(j, vbuf0, sb0, sb1, vop); end();
+    begin(); w.template mphase<false, true>(T, kbuf0, vop, a, b, hq, sa0, sa1, sb0, sb1); end();
+  } else {       // the last tile's scores are in set a
+    begin(); w.template mphase<false, true>(T, kbuf0, vop, a, b, hq, sb0, sb1, sa0, sa1); end();
+  }
+  while (t < 2 * ntiles + 2) { begin(); end(); }
+}
 
 template <int D, int KIND, bool CAUSAL, bool DUMP>
 __global__ __attribute__((amdgpu_flat_work_group_size(kPPThreads, kPPThreads),
@@ -1071,91 +1138,38 @@ attn_pp_kernel(const unsigned short* __restrict__ q, const unsigned short* __res
   w.sel = rowsum_selector(w.lane);
   w.m = -INFINITY;
 
-  // prologue: K(0), K(1), V~(0) resident; K(2), V~(1) in flight
+  // prologue: K(0), K(1), V~(0), V~(1) resident; K(2), V~(2) in flight
   kload.issue(kbuf0, 0, wave);
-  if (ntiles > 1) kload.issue(kbuf0 + Smem<D>::kK, 1, wave);
   vload.issue(vbuf0, 0, wave, w.lane);
+  if (ntiles > 1) {
+    kload.issue(kbuf0 + Smem<D>::kK, 1, wave);
+    vload.issue(vbuf0 + Smem<D>::kV, 1, wave, w.lane);
+  }
   int batch = 0;
   if (ntiles > 2) {
     kload.issue(kbuf0 + 2 * Smem<D>::kK, 2, wave);
-    batch += KLoad<D, kPPWaves>::kIssued;
-  }
-  if (ntiles > 1) {
-    vload.issue(vbuf0 + Smem<D>::kV, 1, wave, w.lane);
-    batch += v_issued;
+    vload.issue(vbuf0 + 2 * Smem<D>::kV, 2, wave, w.lane);
+    batch = KLoad<D, kPPWaves>::kIssued + v_issued;
   }
   wait_vmem_le(batch);
   __syncthreads();
 
-  // Trip j >= 1 streams K(j+2) (replacing K(j-1)) and V~(j+1) (replacing
-  // V~(j-2)); returns the number of loads issued.
+  // Phase 2j (j >= 1) streams K(j+2) (replacing K(j-1)) and V~(j+2)
+  // (replacing V~(j-2)); returns the number of loads issued.
   auto stream = [&](int j) {
     int n = 0;
     if (j + 2 < ntiles) {
       kload.issue(kbuf0 + ((j + 2) % kStages) * Smem<D>::kK, j + 2, wave);
-      n += KLoad<D, kPPWaves>::kIssued;
-    }
-    if (j + 1 < ntiles) {
-      vload.issue(vbuf0 + ((j + 1) % kStages) * Smem<D>::kV, j + 1, wave, w.lane);
-      n += v_issued;
+      vload.issue(vbuf0 + ((j + 2) % kVStages) * Smem<D>::kV, j + 2, wave, w.lane);
+      n = KLoad<D, kPPWaves>::kIssued + v_issued;
     }
     return n;
   };
 
-  // Every wave passes two barriers per trip j = 0 .. ntiles.  The wave's own
-  // tiles run in trips 0 .. wtiles (the first without P~V, the last with
-  // P~V only); later trips only keep the loads and barriers in step.
-  f32x16 s0, s1;
-  VOps<D> vop;
-  u32x4 bop;
-  int sb;
-  // Each loop body ends with a matrix phase, whose results feed the next
-  // trip: this keeps its MFMAs on their side of the barrier.
-  if (group == 0) {
-    w.template mma<false>(0, kbuf0, vop, bop, 0, s0, s1);   // phase 0
-    wg_barrier();
-    for (int j = 1; j < wtiles; ++j) {
-      w.vphase(j - 1, a, b, hq, vbuf0, s0, s1, vop, bop, sb);   // phase 2j-1
-      wait_vmem_le(batch);
-      wg_barrier();
-      batch = stream(j);                                       // phase 2j
-      w.template mma<true>(j, kbuf0, vop, bop, sb, s0, s1);
-      wg_barrier();
-    }
-    w.vphase(wtiles - 1, a, b, hq, vbuf0, s0, s1, vop, bop, sb);
-    wait_vmem_le(batch);
-    wg_barrier();
-    batch = stream(wtiles);
-    w.pv(vop, bop, sb);
-    wg_barrier();
-    wait_vmem_le(batch);
-    wg_barrier();
-  } else {
-    wg_barrier();
-    w.template mma<false>(0, kbuf0, vop, bop, 0, s0, s1);
-    wait_vmem_le(batch);
-    wg_barrier();
-    for (int j = 1; j < wtiles; ++j) {
-      batch = stream(j);
-      w.vphase(j - 1, a, b, hq, vbuf0, s0, s1, vop, bop, sb);
-      wg_barrier();
-      w.template mma<true>(j, kbuf0, vop, bop, sb, s0, s1);
-      wait_vmem_le(batch);
-      wg_barrier();
-    }
-    batch = stream(wtiles);
-    w.vphase(wtiles - 1, a, b, hq, vbuf0, s0, s1, vop, bop, sb);
-    wg_barrier();
-    w.pv(vop, bop, sb);
-    wait_vmem_le(batch);
-    wg_barrier();
-  }
-  for (int j = wtiles + 1; j <= ntiles; ++j) {
-    batch = stream(j);
-    wg_barrier();
-    wait_vmem_le(batch);
-    wg_barrier();
-  }
+  if (group == 0)
+    pp_schedule<0>(w, wtiles, ntiles, kbuf0, vbuf0, a, b, hq, batch, stream);
+  else
+    pp_schedule<1>(w, wtiles, ntiles, kbuf0, vbuf0, a, b, hq, batch, stream);
   wait_vmem();   // no load may still target LDS when the wave leaves
 
   const float l = w.lacc[0];
