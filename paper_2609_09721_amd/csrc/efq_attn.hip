@@ -438,17 +438,16 @@ struct AttnArgs {
 // K and V~ have three buffers each: step j reads K of tile j+1 and V~ of
 // tile j while K of tile j+3 and V~ of tile j+2 stream in, so a load has
 // two steps to land.
-constexpr int kStages = 3;    // K ring depth
-constexpr int kVStages = 4;   // V~ ring depth (the ping-pong kernel streams V~ one tile earlier)
-template <int D>
+constexpr int kStages = 3;    // ring depth of the four-wave kernel
+template <int D, int KS = kStages, int VS = kStages>
 struct Smem {
   static constexpr int kK = kBc * D * 2;                 // one K tile
   static constexpr int kVc = 2 * D * 16;                 // V~ codes of two blocks
   static constexpr int kVs = 256;                        // V~ scales (2 D bytes, padded)
   static constexpr int kV = kVc + kVs;                   // one V~ tile
   static constexpr int kKOff = 0;
-  static constexpr int kVOff = kStages * kK;
-  static constexpr int kTotal = kStages * kK + kVStages * kV;
+  static constexpr int kVOff = KS * kK;
+  static constexpr int kTotal = KS * kK + VS * kV;
 };
 
 // Direct-to-LDS loads (buffer_load ... lds: LDS address = M0 base + size *
@@ -536,7 +535,7 @@ __device__ __forceinline__ void wg_barrier() {
   __builtin_amdgcn_sched_barrier(0);
 }
 // Wait until at most n vector-memory loads of this wave are outstanding
-// (loads complete in issue order); n is wave-uniform and at most 6.
+// (loads complete in issue order); n is wave-uniform and at most 12.
 __device__ __forceinline__ void wait_vmem_le(int n) {
   switch (n) {
     case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
@@ -545,7 +544,13 @@ __device__ __forceinline__ void wait_vmem_le(int n) {
     case 3: asm volatile("s_waitcnt vmcnt(3)" ::: "memory"); break;
     case 4: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
     case 5: asm volatile("s_waitcnt vmcnt(5)" ::: "memory"); break;
-    default: asm volatile("s_waitcnt vmcnt(6)" ::: "memory"); break;
+    case 6: asm volatile("s_waitcnt vmcnt(6)" ::: "memory"); break;
+    case 7: asm volatile("s_waitcnt vmcnt(7)" ::: "memory"); break;
+    case 8: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+    case 9: asm volatile("s_waitcnt vmcnt(9)" ::: "memory"); break;
+    case 10: asm volatile("s_waitcnt vmcnt(10)" ::: "memory"); break;
+    case 11: asm volatile("s_waitcnt vmcnt(11)" ::: "memory"); break;
+    default: asm volatile("s_waitcnt vmcnt(12)" ::: "memory"); break;
   }
 }
 
@@ -901,6 +906,14 @@ __global__ __launch_bounds__(kThreads, EFQ_WAVES_PER_SIMD) void attn_fwd_kernel(
 constexpr int kPPWaves = 8;
 constexpr int kPPBr = kWaveQ * kPPWaves;   // queries per workgroup
 constexpr int kPPThreads = 64 * kPPWaves;
+#ifndef EFQ_PREFETCH
+#define EFQ_PREFETCH 2
+#endif
+constexpr int kPP = EFQ_PREFETCH;          // tiles streamed ahead (>= 2)
+constexpr int kPPK = kPP + 1;              // K ring depth
+constexpr int kPPV = kPP + 2;              // V~ ring depth
+template <int D>
+using SmemPP = Smem<D, kPPK, kPPV>;
 
 // P~1 on the 16x16x128 FP4 MFMA.  Its B operand is the P~^T operand of the
 // P~V product as it sits in the lanes (lane l: query l % 32, key block
@@ -992,13 +1005,14 @@ struct PPWave {
   PgenState st;           // block parameters of the tile between V(j) and M(j+1)
   int lane, half, my_q, vis_end;
 
-  // Matrix phase M(j): with CODES the codes of tile j-1 (scores sc) and its
-  // P~V, P~1; with QK the scores of tile j into sn.
+  // Matrix phase M(j): with QK the scores of tile j into sn, and with CODES
+  // the codes of tile j-1 (scores sc) in the shadow of those MFMAs, then its
+  // P~V and P~1 MFMAs.
   template <bool QK, bool CODES>
   __device__ __forceinline__ void mphase(int j, const uint8_t* kbuf0, const VOps<D>& vop,
                                          const AttnArgs& a, int b, int hq, f32x16& sn0,
                                          f32x16& sn1, const f32x16& sc0, const f32x16& sc1) {
-    const uint8_t* kb = kbuf0 + ((QK ? j : 0) % kStages) * Smem<D>::kK;
+    const uint8_t* kb = kbuf0 + ((QK ? j : 0) % kPPK) * SmemPP<D>::kK;
     PgenOut po = mma_phase<D, KIND, QK, CODES>(kb, qreg, lane, sn0, sn1, sc0, sc1, pa, st);
     if constexpr (CODES) {
       if constexpr (DUMP) {
@@ -1021,7 +1035,7 @@ struct PPWave {
   // and rescale the history when a row maximum moved.
   __device__ __forceinline__ void vphase(int j, const uint8_t* vbuf0, f32x16& s0, f32x16& s1,
                                          VOps<D>& vop) {
-    read_v<D>(vbuf0 + (j % kVStages) * Smem<D>::kV, lane, vop);
+    read_v<D>(vbuf0 + (j % kPPV) * SmemPP<D>::kV, lane, vop);
     const int lim = vis_end - j * kBc;
     if (__builtin_amdgcn_ballot_w64(lim < kBc) != 0ull) mask_tile(s0, s1, lim, half);
     float pm0, pm1;
@@ -1040,26 +1054,39 @@ struct PPWave {
 // and applies its P~V (j >= 1) and F codes and applies the last tile; group
 // G runs op o in phase o + G, so K(j) is read in phases 2j, 2j+1 and V~(j)
 // in phases 2j+1, 2j+2.  Phase t ends with a barrier; even phases t = 2j
-// >= 2 start by streaming K(j+2) and V~(j+2), odd phases end by waiting
-// until only the loads of the even phase before are outstanding (loads
+// >= 2 start by streaming tile j+P (K and V~), odd phases end by waiting
+// until only the loads of the last P-1 even phases are outstanding (loads
 // complete in order).  A load issued in phase 2j has therefore landed by
-// the end of phase 2j+3, in time for K(j+2) in phase 2j+4 and V~(j+2) in
-// phase 2j+5; the slots it overwrites (K(j-1), V~(j-2)) were last read,
-// and the reads consumed, by phase 2j-1.  Every wave passes 2 ntiles + 2
-// barriers.  Scores alternate between two register sets.
+// the end of phase 2(j+P)-1, in time for K(j+P) in phase 2(j+P) and V~(j+P)
+// in phase 2(j+P)+1; the slots it overwrites (K(j-1) in a ring of P+1,
+// V~(j-2) in a ring of P+2) were last read, and the reads consumed, by
+// phase 2j-1.  Every wave passes 2 ntiles + 2 barriers.  Scores alternate
+// between two register sets.
 template <int G, int D, int KIND, bool DUMP, typename Stream>
 __device__ __forceinline__ void pp_schedule(PPWave<D, KIND, DUMP>& w, int T, int ntiles,
                                             const uint8_t* kbuf0, const uint8_t* vbuf0,
-                                            const AttnArgs& a, int b, int hq, int batch,
-                                            Stream stream) {
+                                            const AttnArgs& a, int b, int hq,
+                                            const int (&fifo0)[kPP - 1], Stream stream) {
   f32x16 sa0, sa1, sb0, sb1;
   VOps<D> vop;
+  int fifo[kPP - 1];   // loads issued by the last P-1 even phases, oldest first
+#pragma unroll
+  for (int i = 0; i < kPP - 1; ++i) fifo[i] = fifo0[i];
   int t = 0;   // phase
   auto begin = [&]() {
-    if ((t & 1) == 0 && t >= 2) batch = stream(t >> 1);
+    if ((t & 1) == 0 && t >= 2) {
+#pragma unroll
+      for (int i = 0; i + 1 < kPP - 1; ++i) fifo[i] = fifo[i + 1];
+      fifo[kPP - 2] = stream(t >> 1);
+    }
   };
   auto end = [&]() {
-    if (t & 1) wait_vmem_le(batch);
+    if (t & 1) {
+      int n = 0;
+#pragma unroll
+      for (int i = 0; i < kPP - 1; ++i) n += fifo[i];
+      wait_vmem_le(n);
+    }
     wg_barrier();
     ++t;
   };
@@ -1122,8 +1149,8 @@ attn_pp_kernel(const unsigned short* __restrict__ q, const unsigned short* __res
   VLoad<D, kPPWaves> vload;
   vload.init(vhat + ((long)b * a.Hkv + g) * a.nb * D * 16,
              vhat + a.scale_off + ((long)b * a.Hkv + g) * a.nb * D, a.nb);
-  uint8_t* const kbuf0 = smem + Smem<D>::kKOff;
-  uint8_t* const vbuf0 = smem + Smem<D>::kVOff;
+  uint8_t* const kbuf0 = smem + SmemPP<D>::kKOff;
+  uint8_t* const vbuf0 = smem + SmemPP<D>::kVOff;
   const int v_issued = VLoad<D, kPPWaves>::issued(wave);
 
   w.pa.scale = a.scale;
@@ -1138,38 +1165,35 @@ attn_pp_kernel(const unsigned short* __restrict__ q, const unsigned short* __res
   w.sel = rowsum_selector(w.lane);
   w.m = -INFINITY;
 
-  // prologue: K(0), K(1), V~(0), V~(1) resident; K(2), V~(2) in flight
-  kload.issue(kbuf0, 0, wave);
-  vload.issue(vbuf0, 0, wave, w.lane);
-  if (ntiles > 1) {
-    kload.issue(kbuf0 + Smem<D>::kK, 1, wave);
-    vload.issue(vbuf0 + Smem<D>::kV, 1, wave, w.lane);
+  // Streams tile x (K into ring slot x % (P+1), V~ into x % (P+2)) if it
+  // exists; returns the number of loads issued.
+  auto load_tile = [&](int x) {
+    if (x >= ntiles) return 0;
+    kload.issue(kbuf0 + (x % kPPK) * SmemPP<D>::kK, x, wave);
+    vload.issue(vbuf0 + (x % kPPV) * SmemPP<D>::kV, x, wave, w.lane);
+    return KLoad<D, kPPWaves>::kIssued + v_issued;
+  };
+  // prologue: tiles 0 .. P; tiles 0 and 1 resident, 2 .. P in flight (the
+  // loads of the last P-1 even phases before phase 2)
+  int fifo[kPP - 1];
+  load_tile(0);
+  load_tile(1);
+  int pending = 0;
+#pragma unroll
+  for (int x = 2; x <= kPP; ++x) {
+    fifo[x - 2] = load_tile(x);
+    pending += fifo[x - 2];
   }
-  int batch = 0;
-  if (ntiles > 2) {
-    kload.issue(kbuf0 + 2 * Smem<D>::kK, 2, wave);
-    vload.issue(vbuf0 + 2 * Smem<D>::kV, 2, wave, w.lane);
-    batch = KLoad<D, kPPWaves>::kIssued + v_issued;
-  }
-  wait_vmem_le(batch);
+  wait_vmem_le(pending);
   __syncthreads();
 
-  // Phase 2j (j >= 1) streams K(j+2) (replacing K(j-1)) and V~(j+2)
-  // (replacing V~(j-2)); returns the number of loads issued.
-  auto stream = [&](int j) {
-    int n = 0;
-    if (j + 2 < ntiles) {
-      kload.issue(kbuf0 + ((j + 2) % kStages) * Smem<D>::kK, j + 2, wave);
-      vload.issue(vbuf0 + ((j + 2) % kVStages) * Smem<D>::kV, j + 2, wave, w.lane);
-      n = KLoad<D, kPPWaves>::kIssued + v_issued;
-    }
-    return n;
-  };
+  // phase 2j (j >= 1) streams tile j+P
+  auto stream = [&](int j) { return load_tile(j + kPP); };
 
   if (group == 0)
-    pp_schedule<0>(w, wtiles, ntiles, kbuf0, vbuf0, a, b, hq, batch, stream);
+    pp_schedule<0>(w, wtiles, ntiles, kbuf0, vbuf0, a, b, hq, fifo, stream);
   else
-    pp_schedule<1>(w, wtiles, ntiles, kbuf0, vbuf0, a, b, hq, batch, stream);
+    pp_schedule<1>(w, wtiles, ntiles, kbuf0, vbuf0, a, b, hq, fifo, stream);
   wait_vmem();   // no load may still target LDS when the wave leaves
 
   const float l = w.lacc[0];
@@ -1381,8 +1405,18 @@ template <int D, int KIND, bool CAUSAL, bool DUMP>
 hipError_t launch_attn_t(const void* q, const void* k, const void* vhat, float* out,
                          const AttnArgs& a, hipStream_t st, unsigned grid) {
 #if EFQ_PINGPONG
+  // more dynamic LDS than the default limit: raise it once per kernel (the
+  // call is idempotent, so a race between threads is harmless)
+  static bool lds_ok = false;
+  if (!lds_ok) {
+    hipError_t e = hipFuncSetAttribute((const void*)attn_pp_kernel<D, KIND, CAUSAL, DUMP>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       SmemPP<D>::kTotal);
+    if (e != hipSuccess) return e;
+    lds_ok = true;
+  }
   hipLaunchKernelGGL((attn_pp_kernel<D, KIND, CAUSAL, DUMP>), dim3(grid), dim3(kPPThreads),
-                     Smem<D>::kTotal, st, (const unsigned short*)q, (const unsigned short*)k,
+                     SmemPP<D>::kTotal, st, (const unsigned short*)q, (const unsigned short*)k,
                      (const uint8_t*)vhat, out, a);
 #else
   hipLaunchKernelGGL((attn_fwd_kernel<D, KIND, CAUSAL, DUMP>), dim3(grid), dim3(kThreads),
