@@ -67,7 +67,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="qwen3_8b_16k")
-    ap.add_argument("--kind", default="efq", choices=["efq", "expq", "lut"])
+    ap.add_argument("--kind", default="efq", choices=["efq", "expq", "expq6", "lut"])
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-extra", action="store_true", help="skip the P-gen and policy comparisons")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU oracle time")
@@ -192,7 +192,7 @@ def main():
     if not args.no_extra:
         extra = {}
         # other probability stages in the same fused kernel
-        for kind in ("expq", "noop", "lut"):
+        for kind in ("expq", "expq6", "noop", "lut"):
             if kind == args.kind:
                 continue
             ms_k, attn_k, _, _ = timed(kind, max(5, args.steps // 2), 2)
@@ -202,13 +202,13 @@ def main():
         tiles = w.pairs() / 16384.0            # 128 x 128 score tiles (visible pairs)
         noop = extra["noop"]["attn_ms"]
         exposed = {}
-        for kind in ("efq", "expq", "lut"):
+        for kind in ("efq", "expq", "expq6", "lut"):
             if kind in extra:
                 exposed[kind] = round((extra[kind]["attn_ms"] - noop) * 1e3 * N_CU / tiles, 4)
         # register-resident probe of the probability stage alone
         waves, iters = 8192, 400
         probe = {}
-        for kind in ("efq", "expq", "lut"):
+        for kind in ("efq", "expq", "expq6", "lut"):
             cs = torch.empty(waves, dtype=torch.int32, device=dev)
             binding.pgen_bench(kind, None, waves, 8, cs)
             torch.cuda.synchronize()
@@ -222,8 +222,10 @@ def main():
             probe[kind] = round(ms * 1e3 * N_CU / (scores / 16384.0), 4)
         result["pgen"] = {
             "unit": "us per 128x128 score tile per CU",
-            "probe_efq": probe["efq"], "probe_expq": probe["expq"], "probe_lut": probe["lut"],
+            "probe_efq": probe["efq"], "probe_expq": probe["expq"], "probe_expq6": probe["expq6"],
+            "probe_lut": probe["lut"],
             "probe_speedup": round(1.0 - probe["efq"] / probe["expq"], 4),
+            "probe_speedup_vs_scale6": round(1.0 - probe["efq"] / probe["expq6"], 4),
             "exposed_in_kernel": exposed,
             "exposed_speedup": (round(1.0 - exposed["efq"] / exposed["expq"], 4)
                                 if exposed.get("expq", 0) > 0 else None),

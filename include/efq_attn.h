@@ -78,8 +78,12 @@ enum efq_pgen_kind {
                           fp32 exp, then OCP MXFP4 (scale floor(log2 amax)-2,
                           round to nearest even, saturating)                 */
     EFQ_PGEN_LUT = 2,  /* EFQ-Softmax-LUT, Sec. II-D: 16-level index, C16 fold */
-    EFQ_PGEN_NOOP = 3  /* timing control only: a constant operand, no P-gen
+    EFQ_PGEN_NOOP = 3, /* timing control only: a constant operand, no P-gen
                           work; its output is meaningless                    */
+    EFQ_PGEN_EXPQ6 = 4 /* exp-then-quantize with the "scale6" MXFP4 rule of
+                          the comparison rows of Sec. IV: fp32 exp, scale
+                          2^ceil(log2(amax / 6)) (amax / scale in (3, 6], so
+                          nothing saturates), E2M1 round to nearest even   */
 };
 
 enum efq_status {
@@ -144,7 +148,7 @@ int efq_attn_fwd_expq(const void *q, const void *k, const void *v, float scale, 
  * j) and one E8M0 byte per row and 32-column block (device, rows x
  * ceil(cols/32)).  A partial last block is padded with masked keys.  Runs
  * the same register-level code path as the fused kernel (scale 1, running
- * maximum 0).  kind: EFQ, EXPQ or LUT. */
+ * maximum 0).  kind: EFQ, EXPQ, EXPQ6 or LUT. */
 int efq_pgen(const float *x, int rows, int cols, int kind, efq_params p, uint8_t *codes,
              uint8_t *e8m0, efq_stream_t stream);
 
@@ -163,7 +167,7 @@ int efq_attn_fwd_dump(const void *q, const void *k, const void *vhat, size_t vha
 /* Register-resident P-gen throughput probe: each of `waves` wavefronts
  * (64 lanes, 32 query rows x 64 keys per tile) runs the probability stage of
  * the fused kernel `iters` times on synthetic scores and folds the result
- * into checksum[wave] (device, `waves` uint32).  kind: EFQ, EXPQ or LUT. */
+ * into checksum[wave] (device, `waves` uint32).  kind: EFQ, EXPQ, EXPQ6 or LUT. */
 int efq_pgen_bench(int kind, efq_params p, int waves, int iters, uint32_t *checksum,
                    efq_stream_t stream);
 

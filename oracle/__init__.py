@@ -30,7 +30,7 @@ BALANCE = (-2.10, 2.70)
 # EFQ-Softmax-LUT constants of Sec. II-D: tau16 = log(1/24), h16 = 14/log 24.
 LUT = (float(np.log(1.0 / 24.0)), float(14.0 / np.log(24.0)))
 
-EFQ, EXPQ, EXACT, LUT_MODE = 0, 1, 2, 3
+EFQ, EXPQ, EXACT, LUT_MODE, EXPQ6 = 0, 1, 2, 3, 4
 
 C8 = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])  # Sec. II-B
 C16 = np.array([0, 1, 1, 1, 1, 1, 2, 2, 3, 3, 4, 5, 5, 6, 7, 7])  # Sec. II-D

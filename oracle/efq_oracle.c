@@ -74,7 +74,7 @@ static const double C8[8] = {0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0};
 /* EFQ-Softmax-LUT fold table C16 (Sec. II-D). */
 static const int C16[16] = {0, 1, 1, 1, 1, 1, 2, 2, 3, 3, 4, 5, 5, 6, 7, 7};
 
-enum { ORC_EFQ = 0, ORC_EXPQ = 1, ORC_EXACT = 2, ORC_LUT = 3 };
+enum { ORC_EFQ = 0, ORC_EXPQ = 1, ORC_EXACT = 2, ORC_LUT = 3, ORC_EXPQ6 = 4 };
 
 #define K_MIN (-127) /* smallest E8M0 exponent; 0x00 encodes 2^-127 */
 #define K_MAX 127    /* largest finite E8M0 exponent (0xFE)          */
@@ -232,10 +232,23 @@ static int pgen_block(const float *acc, int n, float scale, float m, float tau,
     return k;
 }
 
+/* Smallest integer k with 6 * 2^k >= a, for a finite a > 0: the "scale6"
+ * exponent ceil(log2(a / 6)), by search from below an exact lower bound. */
+static int ceil_log2_over6(double a)
+{
+    int k = floor_log2(a) - 3; /* 6 * 2^k < 2^(k+3) <= a */
+    while (6.0 * ldexp(1.0, k) < a)
+        ++k;
+    return k;
+}
+
 /* Exp-then-quantize for one block, Eq. (post-softmax-path): p_t = fl32(e^x_t),
- * then the OCP MXFP4 quantiser (scale exponent floor(log2 max p) - 2,
- * elements rounded to nearest even, saturating).  Returns k_b. */
-static int pgen_block_expq(const float *acc, int n, float scale, float m, uint8_t *codes)
+ * then an MXFP4 quantiser with elements rounded to nearest even, saturating.
+ * Scale exponent: the OCP rule floor(log2 max p) - 2, or with scale6 the
+ * rule ceil(log2(max p / 6)) of the paper's MXFP4-scale6 comparison rows
+ * (max p / 2^k in (3, 6], so nothing saturates).  Returns k_b. */
+static int pgen_block_expq(const float *acc, int n, float scale, float m, int scale6,
+                           uint8_t *codes)
 {
     float p[64];
     float amax = 0.0f;
@@ -252,7 +265,8 @@ static int pgen_block_expq(const float *acc, int n, float scale, float m, uint8_
     }
     int k = K_MIN;
     if (amax > 0.0f)
-        k = clampi(floor_log2((double)amax) - 2, K_MIN, K_MAX);
+        k = clampi(scale6 ? ceil_log2_over6((double)amax) : floor_log2((double)amax) - 2,
+                   K_MIN, K_MAX);
     for (int t = 0; t < n; ++t)
         codes[t] = (uint8_t)e2m1_nearest(ldexp((double)p[t], -k));
     return k;
@@ -262,7 +276,8 @@ static int pgen_block_expq(const float *acc, int n, float scale, float m, uint8_
  * Standalone P-gen unit (Sec. III-D kernel interface): shifted scores x
  * (rows x cols, row-major, -inf = masked) -> codes (one per byte) and one
  * E8M0 byte (k_b + 127) per 32-column block.  The last block of a row may
- * be partial (cols not a multiple of 32).  mode: ORC_EFQ, ORC_LUT, ORC_EXPQ.
+ * be partial (cols not a multiple of 32).  mode: ORC_EFQ, ORC_LUT, ORC_EXPQ,
+ * ORC_EXPQ6.
  * Here x is the score itself: scale 1 and row maximum 0.
  * ---------------------------------------------------------------------- */
 int orc_pgen(const float *x, long rows, int cols, int mode, float tau, float h,
@@ -278,8 +293,8 @@ int orc_pgen(const float *x, long rows, int cols, int mode, float tau, float h,
             const float *xb = x + r * (long)cols + t0;
             uint8_t *cb = codes + r * (long)cols + t0;
             int k;
-            if (mode == ORC_EXPQ)
-                k = pgen_block_expq(xb, n, 1.0f, 0.0f, cb);
+            if (mode == ORC_EXPQ || mode == ORC_EXPQ6)
+                k = pgen_block_expq(xb, n, 1.0f, 0.0f, mode == ORC_EXPQ6, cb);
             else
                 k = pgen_block(xb, n, 1.0f, 0.0f, tau, h, mode == ORC_LUT, cb, NULL);
             e8m0[r * nblk + b] = (uint8_t)(k + 127);
@@ -395,7 +410,8 @@ static double e2m1_value(uint8_t c, int k)
  * reads key/value head hq / (Hq/Hkv).  causal (requires Sq == Sk): key t is
  * visible to query i iff t <= i.  Keys t >= Sk are padding (masked).
  * rows: nrows triples (b, hq, i).  out: [nrows][D] fp32.
- * mode ORC_EFQ / ORC_LUT: P from Alg. 1, V as MXFP4.  ORC_EXPQ: P from the
+ * mode ORC_EFQ / ORC_LUT: P from Alg. 1, V as MXFP4.  ORC_EXPQ (ORC_EXPQ6,
+ * scale6 rule): P from the
  * exp-then-quantize path, V as MXFP4.  ORC_EXACT: fp64 softmax with
  * unquantised V (the unquantised reference of the calibration objective).
  * Optional dumps (may be NULL): codes [nrows][nblk*32] (one code per byte),
@@ -546,8 +562,8 @@ int orc_attn(const uint16_t *q, const uint16_t *kmat, const uint16_t *v, int B, 
              * denominator-basic) from the same operand. */
             for (int b0 = 0; b0 < bc; b0 += 32) {
                 int kb;
-                if (mode == ORC_EXPQ)
-                    kb = pgen_block_expq(acc + b0, 32, scale, mnew, cd + b0);
+                if (mode == ORC_EXPQ || mode == ORC_EXPQ6)
+                    kb = pgen_block_expq(acc + b0, 32, scale, mnew, mode == ORC_EXPQ6, cd + b0);
                 else
                     kb = pgen_block(acc + b0, 32, scale, mnew, tau, h, mode == ORC_LUT,
                                     cd + b0, row_margin ? &margin : NULL);

@@ -16,8 +16,9 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libefq_attn.so")
 
-PGEN_EFQ, PGEN_EXPQ, PGEN_LUT, PGEN_NOOP = 0, 1, 2, 3
-KINDS = {"efq": PGEN_EFQ, "expq": PGEN_EXPQ, "lut": PGEN_LUT, "noop": PGEN_NOOP}
+PGEN_EFQ, PGEN_EXPQ, PGEN_LUT, PGEN_NOOP, PGEN_EXPQ6 = 0, 1, 2, 3, 4
+KINDS = {"efq": PGEN_EFQ, "expq": PGEN_EXPQ, "lut": PGEN_LUT, "noop": PGEN_NOOP,
+         "expq6": PGEN_EXPQ6}
 
 # (tau, h) operating points of Sec. IV-A, and the LUT constants of Sec. II-D
 PARAMS_MEAN = (-3.06, 2.30)

@@ -168,6 +168,10 @@ __device__ __forceinline__ void pg_max(const f32x16& s0, const f32x16& s1, float
   }
 }
 
+// The exp-then-quantize baselines (OCP floor rule and the scale6 rule).
+template <int KIND>
+constexpr bool is_expq() { return KIND == EFQ_PGEN_EXPQ || KIND == EFQ_PGEN_EXPQ6; }
+
 template <int KIND>
 __device__ __forceinline__ void pg_params(float pm0, float pm1, float& m, const PgenArgs& pa,
                                           PgenState& st) {
@@ -177,7 +181,7 @@ __device__ __forceinline__ void pg_params(float pm0, float pm1, float& m, const 
     st.w[0] = st.w[1] = st.w[2] = st.w[3] = 0x22222222u;
     return;
   } else {
-    constexpr bool LOG2 = (KIND == EFQ_PGEN_EXPQ);
+    constexpr bool LOG2 = is_expq<KIND>();
     const float unit = LOG2 ? pa.l2s : pa.scale;
     swap32f(pm0, pm1);                          // lower: (own, partner) block 0; upper: block 1
     const float bmine = __builtin_fmaxf(pm0, pm1);   // raw maximum of the lane's own block
@@ -189,13 +193,17 @@ __device__ __forceinline__ void pg_params(float pm0, float pm1, float& m, const 
     const float d = LOG2 ? (m - mnew) : (m - mnew) * kInvLn2;
     st.alpha = (m == mnew) ? 1.0f : __builtin_amdgcn_exp2f(d);
     m = mnew;
-    if constexpr (KIND == EFQ_PGEN_EXPQ) {
+    if constexpr (is_expq<KIND>()) {
       // exp-then-quantize, Eq. (post-softmax-path): max_t exp(x_t) =
       // exp(max_t x_t); the shift S2 - m2 is exact at the row maximum, so it
       // gets p = 1 exactly (an fma of the unshifted score could land on the
       // wrong side of the power-of-two scale boundary)
       const float amax = __builtin_amdgcn_exp2f(bmine * pa.l2s - m);
-      int kb = (int)((__float_as_uint(amax) >> 23) & 0xFF) - 127 - 2;
+      const unsigned ab = __float_as_uint(amax);
+      // OCP: floor(log2 amax) - 2; scale6: ceil(log2(amax / 6)), which is
+      // floor(log2 amax) - 2, plus one when the mantissa exceeds 1.5
+      int kb = (int)((ab >> 23) & 0xFF) - 127 - 2;
+      if constexpr (KIND == EFQ_PGEN_EXPQ6) kb += (ab & 0x7FFFFF) > 0x400000u ? 1 : 0;
       kb = kb < -126 ? -126 : kb;               // 2^k must be a normal fp32 scale
       unsigned k0 = (unsigned)(kb + 127), k1 = k0;
       swap32(k0, k1);                           // (E8M0 of block 0, of block 1)
@@ -255,7 +263,7 @@ __device__ __forceinline__ void pg_pair(const f32x16& s0, const f32x16& s1, cons
   if constexpr (KIND != EFQ_PGEN_NOOP) {
     constexpr int WIN = E / 16, R = E % 16, DW = E / 8, J = E % 8;
     const f32x16& s = WIN ? s1 : s0;
-    if constexpr (KIND == EFQ_PGEN_EXPQ) {
+    if constexpr (is_expq<KIND>()) {
       // RNE(p / 2^k) to E2M1 with saturation; elements j and j + 4 share
       // byte j, so the pair is converted once both are known
       if constexpr (J < 4) {
@@ -884,7 +892,7 @@ __global__ __launch_bounds__(kThreads, EFQ_WAVES_PER_SIMD) void attn_fwd_kernel(
     if constexpr (DUMP) {
       long row = ((long)b * a.Hq + hq) * a.Sq + w.my_q;
       if (w.half == 0) {
-        a.row_m[row] = KIND == EFQ_PGEN_EXPQ ? w.m * kLn2 : w.m;
+        a.row_m[row] = is_expq<KIND>() ? w.m * kLn2 : w.m;
         a.row_l[row] = l;
       }
     }
@@ -1212,7 +1220,7 @@ attn_pp_kernel(const unsigned short* __restrict__ q, const unsigned short* __res
     if constexpr (DUMP) {
       long row = ((long)b * a.Hq + hq) * a.Sq + w.my_q;
       if (w.half == 0) {
-        a.row_m[row] = KIND == EFQ_PGEN_EXPQ ? w.m * kLn2 : w.m;
+        a.row_m[row] = is_expq<KIND>() ? w.m * kLn2 : w.m;
         a.row_l[row] = l;
       }
     }
@@ -1437,6 +1445,7 @@ hipError_t launch_attn_d(int kind, bool causal, const void* q, const void* k, co
     EFQ_CASE(EFQ_PGEN_EFQ)
     EFQ_CASE(EFQ_PGEN_EXPQ)
     EFQ_CASE(EFQ_PGEN_LUT)
+    EFQ_CASE(EFQ_PGEN_EXPQ6)
     default:
       break;
   }
@@ -1484,7 +1493,9 @@ int launch_attn(const void* q, const void* k, const void* vhat, float scale, int
 }
 
 int check_kind(int kind, bool allow_noop) {
-  if (kind == EFQ_PGEN_EFQ || kind == EFQ_PGEN_EXPQ || kind == EFQ_PGEN_LUT) return EFQ_OK;
+  if (kind == EFQ_PGEN_EFQ || kind == EFQ_PGEN_EXPQ || kind == EFQ_PGEN_LUT ||
+      kind == EFQ_PGEN_EXPQ6)
+    return EFQ_OK;
   if (allow_noop && kind == EFQ_PGEN_NOOP) return EFQ_OK;
   return fail(EFQ_EINVAL, "unknown or disallowed P-gen kind %d", kind);
 }
@@ -1642,6 +1653,8 @@ int efq_pgen(const float* x, int rows, int cols, int kind, efq_params p, uint8_t
     hipLaunchKernelGGL(pgen_kernel<EFQ_PGEN_EFQ>, grid, dim3(64), 0, st, x, codes, e8m0, a);
   else if (kind == EFQ_PGEN_LUT)
     hipLaunchKernelGGL(pgen_kernel<EFQ_PGEN_LUT>, grid, dim3(64), 0, st, x, codes, e8m0, a);
+  else if (kind == EFQ_PGEN_EXPQ6)
+    hipLaunchKernelGGL(pgen_kernel<EFQ_PGEN_EXPQ6>, grid, dim3(64), 0, st, x, codes, e8m0, a);
   else
     hipLaunchKernelGGL(pgen_kernel<EFQ_PGEN_EXPQ>, grid, dim3(64), 0, st, x, codes, e8m0, a);
   hipError_t e = hipGetLastError();
@@ -1664,6 +1677,9 @@ int efq_pgen_bench(int kind, efq_params p, int waves, int iters, uint32_t* check
   else if (kind == EFQ_PGEN_LUT)
     hipLaunchKernelGGL(pgen_bench_kernel<EFQ_PGEN_LUT>, grid, dim3(256), 0, st, iters, p.tau, p.h,
                        checksum, waves);
+  else if (kind == EFQ_PGEN_EXPQ6)
+    hipLaunchKernelGGL(pgen_bench_kernel<EFQ_PGEN_EXPQ6>, grid, dim3(256), 0, st, iters, p.tau,
+                       p.h, checksum, waves);
   else
     hipLaunchKernelGGL(pgen_bench_kernel<EFQ_PGEN_EXPQ>, grid, dim3(256), 0, st, iters, p.tau, p.h,
                        checksum, waves);

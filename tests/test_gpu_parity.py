@@ -97,14 +97,17 @@ def test_pgen_random_bitexact(B, orc):
     assert np.array_equal(unpack(cg.cpu().numpy()), co)
 
 
-def test_pgen_expq_close(B, orc):
-    """Exp-then-quantize: the GPU's exp is not correctly rounded, so codes may
-    differ at round-to-nearest midpoints only."""
+@pytest.mark.parametrize("kind", ["expq", "expq6"])
+def test_pgen_expq_close(B, orc, kind):
+    """Exp-then-quantize (OCP and scale6 rules): the GPU's exp is not
+    correctly rounded, so codes and scales may differ at rounding
+    midpoints and scale boundaries only."""
     rng = np.random.default_rng(3)
     x = -rng.exponential(3.0, size=(2048, 256)).astype(np.float32)
     x[:, ::32] = np.minimum(x[:, ::32], -1e-3)
-    cg, eg = B.pgen(torch.from_numpy(x).cuda(), "expq")
-    co, eo = orc.pgen(x, orc.EXPQ)
+    x[7, :32] = 0.0                       # row maximum p = 1 in a block
+    cg, eg = B.pgen(torch.from_numpy(x).cuda(), kind)
+    co, eo = orc.pgen(x, orc.EXPQ if kind == "expq" else orc.EXPQ6)
     cg = unpack(cg.cpu().numpy())
     assert np.mean(eg.cpu().numpy() == eo) > 0.9999
     assert np.mean(cg == co) > 0.9999
@@ -167,14 +170,16 @@ def test_attn_dump_exact_scores(B, orc, case, kind):
 
 
 @pytest.mark.parametrize("case", CASES[:3])
-def test_attn_expq_exact_scores(B, orc, case):
+@pytest.mark.parametrize("kind", ["expq", "expq6"])
+def test_attn_expq_exact_scores(B, orc, case, kind):
     Bt, Sq, Sk, Hq, Hkv, D, causal = case
     w = inputs.Workload("d", Bt, Hq, Hkv, max(Sq, Sk), D, causal, "dyadic", 21 + Sq)
     q, k, v = inputs.dyadic_qkv(w)
     vh = B.quant_v(v.cuda(), seq_q=Sq, heads_q=Hq)
-    out, codes, e8, rm, rl = B.attn_fwd_dump(q.cuda(), k.cuda(), vh, w.scale, causal, "expq")
+    out, codes, e8, rm, rl = B.attn_fwd_dump(q.cuda(), k.cuda(), vh, w.scale, causal, kind)
+    mode = orc.EXPQ if kind == "expq" else orc.EXPQ6
     oo, co, eo, mo, lo = orc.attn(orc.bf16_bits(q), orc.bf16_bits(k), orc.bf16_bits(v), w.scale,
-                                  causal, orc.EXPQ, bc=64, dump=True)
+                                  causal, mode, bc=64, dump=True)
     nblk = (Sk + 31) // 32
     cg = unpack(codes.cpu().numpy()).reshape(-1, nblk * 32)
     assert np.mean(cg == co) > 1 - 1e-4
@@ -186,7 +191,8 @@ def test_tiny_config_all_rows(B, orc):
     """The tiny workload (1 x 256 x 64, N(0,1)), every row."""
     w = inputs.WORKLOADS["tiny"]
     q, k, v = inputs.make_qkv(w)
-    for kind, mode in [("efq", orc.EFQ), ("expq", orc.EXPQ), ("lut", orc.LUT_MODE)]:
+    for kind, mode in [("efq", orc.EFQ), ("expq", orc.EXPQ), ("lut", orc.LUT_MODE),
+                       ("expq6", orc.EXPQ6)]:
         out = B.attn_fwd(q.cuda(), k.cuda(), v.cuda(), w.scale, w.causal, kind)
         oo = orc.attn(orc.bf16_bits(q), orc.bf16_bits(k), orc.bf16_bits(v), w.scale, w.causal, mode)
         og = out.cpu().numpy().transpose(0, 2, 1, 3).reshape(-1, w.head_dim)
@@ -210,6 +216,6 @@ def test_same_operand_v_constant(B):
     q, k, v = inputs.make_qkv(w)
     for c in (1.0, -3.0):
         vc = torch.full_like(v, c)
-        for kind in ("efq", "expq", "lut"):
+        for kind in ("efq", "expq", "lut", "expq6"):
             out = B.attn_fwd(q.cuda(), k.cuda(), vc.cuda(), w.scale, True, kind)
             assert float((out - c).abs().max()) <= 1e-6 * abs(c) * 8

@@ -282,6 +282,46 @@ def test_expq_definition(orc):
     assert np.all(err <= step + 1e-12)
 
 
+def test_expq_scale6_definition(orc):
+    """The scale6 comparison rule: 2^k is the smallest power of two with
+    6 * 2^k >= max p, so max p / 2^k lies in (3, 6] and no element
+    saturates; the row maximum p = 1 gets k = -2 (1 / 2^-2 = 4, code 6);
+    a block max just above 6 * 2^j moves k to j + 1; each element is the
+    nearest E2M1 value."""
+    rng = np.random.default_rng(12)
+    M = rng.uniform(-20, 0, 20000).astype(np.float32)
+    x = blocks_with_max(rng, M)
+    x[0, 0] = 0.0
+    codes, e8 = orc.pgen(x, orc.EXPQ6)
+    k = e8[:, :1].astype(np.float64) - 127
+    assert codes[0, 0] == 6 and e8[0, 0] == 125            # 1 = 4 * 2^-2
+    p = np.exp(x.astype(np.float32).astype(np.float64)).astype(np.float32).astype(np.float64)
+    y = p / 2.0 ** k
+    ymax = y.max(axis=1)
+    assert np.all((ymax > 3) & (ymax <= 6))
+    # the scale is the smallest power of two that keeps the block max <= 6
+    assert np.all(p.max(axis=1) / 2.0 ** (k[:, 0] - 1) > 6)
+    grid = np.array(orc.C8)
+    err = np.abs(grid[codes] - y)
+    step = np.where(y < 2, 0.25, np.where(y < 4, 0.5, 1.0))
+    assert np.all(err <= step + 1e-12)
+    # boundary: p_max = 6 * 2^-3 = 0.75 exactly gives k = -3 (ratio 6, code 7);
+    # the next fp32 value above it gives k = -2 (ratio just above 3, code 5)
+    for pm, kk, c in [(0.75, -3, 7), (float(np.nextafter(np.float32(0.75), np.float32(1))), -2, 5)]:
+        xb = np.full((1, 32), -np.inf, np.float32)
+        # a score whose fp32 exp is pm: search the float32 neighbourhood of log(pm)
+        s0 = np.float32(np.log(pm))
+        cand = [s0]
+        for _ in range(4):
+            cand += [np.nextafter(cand[-1], np.float32(-np.inf))]
+        cand += [np.nextafter(s0, np.float32(np.inf))]
+        hit = [v for v in cand if np.float32(np.exp(np.float64(v))) == np.float32(pm)]
+        assert hit, pm
+        xb[0, 0] = hit[0]
+        cb, eb = orc.pgen(xb, orc.EXPQ6)
+        assert int(eb[0, 0]) - 127 == kk and int(cb[0, 0]) == c, (pm, eb, cb)
+
+
 # ------------------------------------------------------------- V quantiser
 def _bits(t):
     return t.view(torch.int16).numpy().view(np.uint16)
