@@ -28,7 +28,8 @@
  *    (ragged tails are masked).  batch * heads_q * ceil(seq_q / 128) must fit
  *    in a 32-bit grid.
  *  - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
- *    stream) and never synchronise the host.  The caller owns every buffer;
+ *    stream) and never synchronise the host (efq_calibrate excepted).  The
+ *    caller owns every buffer;
  *    the library keeps no allocation beyond its code objects, except that the
  *    convenience entry points without a workspace argument take one
  *    stream-ordered allocation for V~ and release it on the same stream.
@@ -137,6 +138,31 @@ int efq_attn_fwd(const void *q, const void *k, const void *v, float scale, int c
                  float *out, const efq_shape *s, efq_stream_t stream);
 int efq_attn_fwd_expq(const void *q, const void *k, const void *v, float scale, int causal,
                       float *out, const efq_shape *s, efq_stream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * Offline selection of (tau, h), Algorithm 3 and Sec. III-C: for every
+ * candidate pair (taus[i], hs[j]), i outer and j inner, run the EFQ attention
+ * forward on the calibration inputs and compute
+ *   rho(tau, h) = ||O~(tau, h) - O_ref||_F / ||O_ref||_F
+ * (sums of squares in fp64, reduced in a fixed order).  *best receives the
+ * first pair with the smallest rho (a later pair replaces it only when
+ * strictly smaller), rho (host, may be NULL) the [ntau][nh] objective grid.
+ *   q, k, v   device, as for efq_attn_fwd (the calibration inputs)
+ *   o_ref     device fp32 [batch][seq_q][heads_q][head_dim]: the reference
+ *             output (e.g. exact softmax attention); it must not be all zero
+ *   taus, hs  host arrays of ntau and nh candidates (finite, h > 0),
+ *             at most 65536 pairs
+ *   ws        device workspace of efq_calibrate_workspace_bytes(s, ntau*nh)
+ *             bytes, 256-byte aligned, or NULL with ws_bytes == 0 (then one
+ *             stream-ordered allocation is taken and released)
+ * Unlike the other entry points this call waits for `stream` to finish
+ * (the selection needs the objective values on the host).
+ * ------------------------------------------------------------------------- */
+size_t efq_calibrate_workspace_bytes(const efq_shape *s, int ncand);
+int efq_calibrate(const void *q, const void *k, const void *v, float scale, int causal,
+                  const float *o_ref, const efq_shape *s, const float *taus, int ntau,
+                  const float *hs, int nh, double *rho, efq_params *best, void *ws,
+                  size_t ws_bytes, efq_stream_t stream);
 
 /* ---------------------------------------------------------------------------
  * Diagnostics.

@@ -180,6 +180,31 @@ def attn(q_bits, k_bits, v_bits, scale: float, causal: bool, mode: int = EFQ,
     return res if len(res) > 1 else out
 
 
+
+def calibrate(q_bits, k_bits, v_bits, scale: float, causal: bool, o_ref: np.ndarray, taus, hs,
+              bc: int = 64, nthreads: int = 0):
+    """Algorithm 3 (offline selection of (tau, h), Sec. III-C): for every
+    candidate pair, tau outer and h inner, run EFQ attention on all rows and
+    compute rho = ||O~ - O_ref||_F / ||O_ref||_F in fp64; keep the first pair
+    with a strictly smaller rho.  o_ref: [B*Hq*Sq, D] in all_rows order.
+    Candidates are used as fp32 values.  Returns ((tau*, h*), rho [nt, nh])."""
+    taus = [np.float32(t) for t in taus]
+    hs = [np.float32(x) for x in hs]
+    ref = np.asarray(o_ref, np.float64)
+    ref_norm = np.sqrt(np.sum(ref * ref))
+    rho = np.zeros((len(taus), len(hs)))
+    best, best_rho = None, np.inf
+    for i, tau in enumerate(taus):
+        for j, h in enumerate(hs):
+            o = attn(q_bits, k_bits, v_bits, scale, causal, EFQ, tau=float(tau), h=float(h), bc=bc,
+                     nthreads=nthreads).astype(np.float64)
+            d = o - ref
+            r = np.sqrt(np.sum(d * d)) / ref_norm
+            rho[i, j] = r
+            if r < best_rho:
+                best_rho, best = r, (float(tau), float(h))
+    return best, rho
+
 def bf16_bits(t) -> np.ndarray:
     """Bit patterns of a bf16 torch tensor as a uint16 numpy array (a view of
     the same values; no arithmetic)."""

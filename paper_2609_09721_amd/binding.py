@@ -65,6 +65,8 @@ SIGNATURES = {
     "efq_pgen": ([P, I, I, I, Params, P, P, P], I),
     "efq_attn_fwd_dump": ([P, P, P, SZ, F, I, I, Params, P, SP, P, P, P, P, P], I),
     "efq_pgen_bench": ([I, Params, I, I, P, P], I),
+    "efq_calibrate_workspace_bytes": ([SP, I], SZ),
+    "efq_calibrate": ([P, P, P, F, I, P, SP, P, I, P, I, P, ctypes.POINTER(Params), P, SZ, P], I),
 }
 
 
@@ -219,6 +221,36 @@ def attn_fwd_dump(q, k, vhat, scale=None, causal=False, kind="efq", params=None,
                                    _ptr(row_l), _stream(stream)))
     return out, codes, e8, row_m, row_l
 
+
+
+def calibrate(q, k, v, o_ref, taus, hs, scale: Optional[float] = None, causal: bool = False,
+              stream=None):
+    """Algorithm 3 on the GPU: returns ((tau*, h*), rho [len(taus), len(hs)]).
+
+    q, k, v: bf16 BSHD device tensors (calibration inputs); o_ref: fp32
+    reference output of the shape of q.  Waits for the stream."""
+    import numpy as np
+    _bf16(q, "q")
+    _bf16(k, "k")
+    _bf16(v, "v")
+    if o_ref.dtype != torch.float32 or o_ref.shape != q.shape or not o_ref.is_contiguous():
+        raise ValueError("o_ref must be a contiguous fp32 tensor of the shape of q")
+    sh = shape_of(q, k)
+    if scale is None:
+        scale = q.shape[-1] ** -0.5
+    ta = np.ascontiguousarray(taus, dtype=np.float32)
+    ha = np.ascontiguousarray(hs, dtype=np.float32)
+    rho = np.zeros((len(ta), len(ha)), np.float64)
+    best = Params(0.0, 0.0)
+    nbytes = lib().efq_calibrate_workspace_bytes(ctypes.byref(sh), len(ta) * len(ha))
+    ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=q.device)
+    off = (-ws.data_ptr()) % 256
+    _check(lib().efq_calibrate(_ptr(q), _ptr(k), _ptr(v), float(scale), int(causal), _ptr(o_ref),
+                               ctypes.byref(sh), ta.ctypes.data_as(ctypes.c_void_p), len(ta),
+                               ha.ctypes.data_as(ctypes.c_void_p), len(ha),
+                               rho.ctypes.data_as(ctypes.c_void_p), ctypes.byref(best),
+                               ctypes.c_void_p(ws.data_ptr() + off), nbytes, _stream(stream)))
+    return (best.tau, best.h), rho
 
 def pgen(x: torch.Tensor, kind="efq", params=None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
     """P-gen unit on shifted scores x [rows, cols] fp32 (CUDA)."""

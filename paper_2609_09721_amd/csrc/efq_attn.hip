@@ -29,6 +29,7 @@
 #include <mutex>
 #include <type_traits>
 #include <utility>
+#include <vector>
 
 #include "efq_attn.h"
 
@@ -1316,6 +1317,64 @@ __global__ void fill_zero_kernel(uint8_t* __restrict__ p, size_t n) {
   for (; i < n; i += stride) p[i] = 0;
 }
 
+// ------------------------------------------------ calibration objective
+// rho(tau, h) = ||O~ - O_ref||_F / ||O_ref||_F (Sec. III-C, Alg. 3): sums of
+// squares in fp64, reduced in a fixed order (per-block partials, then one
+// block), so repeated runs give identical values.
+constexpr int kRhoBlocks = 1024;
+
+__global__ __launch_bounds__(256) void rho_partial_kernel(const float* __restrict__ o,
+                                                          const float* __restrict__ r, long n,
+                                                          double* __restrict__ part) {
+  double d2 = 0.0, r2 = 0.0;
+  for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < n; i += (long)gridDim.x * 256) {
+    const double a = o[i], b = r[i];
+    d2 += (a - b) * (a - b);
+    r2 += b * b;
+  }
+  __shared__ double s1[256], s2[256];
+  s1[threadIdx.x] = d2;
+  s2[threadIdx.x] = r2;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) {
+      s1[threadIdx.x] += s1[threadIdx.x + w];
+      s2[threadIdx.x] += s2[threadIdx.x + w];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    part[2 * blockIdx.x] = s1[0];
+    part[2 * blockIdx.x + 1] = s2[0];
+  }
+}
+
+// One block: the kRhoBlocks partial pairs -> res[0] = sum (O~ - O_ref)^2,
+// res[1] = sum O_ref^2.
+__global__ __launch_bounds__(256) void rho_final_kernel(const double* __restrict__ part,
+                                                        double* __restrict__ res) {
+  __shared__ double s1[256], s2[256];
+  double a = 0.0, b = 0.0;
+  for (int i = threadIdx.x; i < kRhoBlocks; i += 256) {
+    a += part[2 * i];
+    b += part[2 * i + 1];
+  }
+  s1[threadIdx.x] = a;
+  s2[threadIdx.x] = b;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) {
+      s1[threadIdx.x] += s1[threadIdx.x + w];
+      s2[threadIdx.x] += s2[threadIdx.x + w];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    res[0] = s1[0];
+    res[1] = s2[0];
+  }
+}
+
 // ================================================================ host side
 #if EFQ_PINGPONG
 constexpr int kQTile = kPPBr;   // queries per workgroup of the launched kernel
@@ -1603,6 +1662,90 @@ int efq_attn_fwd_expq(const void* q, const void* k, const void* v, float scale, 
                       float* out, const efq_shape* s, efq_stream_t stream) {
   return efq_attn_fwd_ex(q, k, v, scale, causal, EFQ_PGEN_EXPQ, efq_params{EFQ_TAU_MEAN, EFQ_H_MEAN},
                          out, s, nullptr, 0, stream);
+}
+
+// Workspace of efq_calibrate: V~, one output, the reduction partials and
+// one result pair per candidate, each 256-byte aligned.
+static size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
+
+size_t efq_calibrate_workspace_bytes(const efq_shape* s, int ncand) {
+  if (!s || ncand < 1 || validate_shape(s, 0) != EFQ_OK) return 0;
+  const size_t out = (size_t)s->batch * s->seq_q * s->heads_q * s->head_dim * 4;
+  return align256(vhat_bytes(s)) + align256(out) + align256((size_t)kRhoBlocks * 16) +
+         align256((size_t)ncand * 16);
+}
+
+int efq_calibrate(const void* q, const void* k, const void* v, float scale, int causal,
+                  const float* o_ref, const efq_shape* s, const float* taus, int ntau,
+                  const float* hs, int nh, double* rho, efq_params* best, void* ws,
+                  size_t ws_bytes, efq_stream_t stream) {
+  int rc = validate_shape(s, causal);
+  if (rc) return rc;
+  if (!q || !k || !v || !o_ref || !taus || !hs || !best) return fail(EFQ_EINVAL, "null pointer");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o_ref))
+    return fail(EFQ_EINVAL, "pointers must be 16-byte aligned");
+  if (ntau < 1 || nh < 1 || (long)ntau * nh > 65536)
+    return fail(EFQ_EINVAL, "candidate sets must be non-empty (at most 65536 pairs)");
+  if ((rc = check_scale(scale))) return rc;
+  for (int i = 0; i < ntau; ++i)
+    for (int j = 0; j < nh; ++j)
+      if ((rc = check_params(efq_params{taus[i], hs[j]}))) return rc;
+  const int nc = ntau * nh;
+  const size_t need = efq_calibrate_workspace_bytes(s, nc);
+  if (ws_bytes != 0 && (!ws || ws_bytes < need))
+    return fail(EFQ_EWORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  if (ws && ((uintptr_t)ws & 255)) return fail(EFQ_EINVAL, "workspace must be 256-byte aligned");
+  if ((rc = check_device())) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  uint8_t* buf = (uint8_t*)ws;
+  if (ws_bytes == 0) {
+    hipError_t e = hipMallocAsync((void**)&buf, need, st);
+    if (e != hipSuccess) return fail(EFQ_EHIP, "hipMallocAsync(%zu): %s", need, hipGetErrorString(e));
+  }
+  uint8_t* vhat = buf;
+  float* out = (float*)(buf + align256(vhat_bytes(s)));
+  const long n = (long)s->batch * s->seq_q * s->heads_q * s->head_dim;
+  double* part = (double*)((uint8_t*)out + align256((size_t)n * 4));
+  double* res = (double*)((uint8_t*)part + align256((size_t)kRhoBlocks * 16));
+  // Alg. 3: every (tau, h), tau outer, on the same inputs and V~
+  rc = launch_vquant(v, s, vhat, st);
+  for (int c = 0; c < nc && rc == EFQ_OK; ++c) {
+    const efq_params p{taus[c / nh], hs[c % nh]};
+    rc = launch_attn(q, k, vhat, scale, causal, EFQ_PGEN_EFQ, p, out, s, st, nullptr, nullptr,
+                     nullptr, nullptr);
+    if (rc != EFQ_OK) break;
+    hipLaunchKernelGGL(rho_partial_kernel, dim3(kRhoBlocks), dim3(256), 0, st, out, o_ref, n, part);
+    hipLaunchKernelGGL(rho_final_kernel, dim3(1), dim3(256), 0, st, part, res + 2 * c);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) rc = fail(EFQ_EHIP, "calibration launch: %s", hipGetErrorString(e));
+  }
+  std::vector<double> sums((size_t)nc * 2);
+  if (rc == EFQ_OK) {
+    hipError_t e = hipMemcpyAsync(sums.data(), res, sums.size() * sizeof(double),
+                                  hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) rc = fail(EFQ_EHIP, "calibration readback: %s", hipGetErrorString(e));
+  }
+  if (ws_bytes == 0) {
+    hipError_t e = hipFreeAsync(buf, st);
+    if (rc == EFQ_OK && e != hipSuccess) rc = fail(EFQ_EHIP, "hipFreeAsync: %s", hipGetErrorString(e));
+  }
+  if (rc != EFQ_OK) return rc;
+  if (!(sums[1] > 0.0)) return fail(EFQ_EINVAL, "reference output is zero");
+  // Alg. 3: keep the first pair with a strictly smaller objective
+  double best_rho = INFINITY;
+  int best_c = 0;
+  for (int c = 0; c < nc; ++c) {
+    const double r = std::sqrt(sums[2 * c]) / std::sqrt(sums[2 * c + 1]);
+    if (rho) rho[c] = r;
+    if (r < best_rho) {
+      best_rho = r;
+      best_c = c;
+    }
+  }
+  best->tau = taus[best_c / nh];
+  best->h = hs[best_c % nh];
+  return EFQ_OK;
 }
 
 int efq_attn_fwd_dump(const void* q, const void* k, const void* vhat, size_t vhat_nbytes,

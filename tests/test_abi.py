@@ -103,6 +103,32 @@ def test_bad_arguments(L):
                                ctypes.byref(s), None, 64, None) == L.EFQ_EWORKSPACE
 
 
+def test_calibrate_arguments(L):
+    """Alg. 3 entry point: every argument error is reported before any HIP call."""
+    import numpy as np
+    s = shape()
+    lib = L.lib()
+    taus = np.array([-3.06, -2.9], np.float32)
+    hs = np.array([2.3, 2.0], np.float32)
+    T = taus.ctypes.data_as(ctypes.c_void_p)
+    H = hs.ctypes.data_as(ctypes.c_void_p)
+    best = L.Params(0, 0)
+    need = lib.efq_calibrate_workspace_bytes(ctypes.byref(s), 4)
+    assert need > L.vhat_bytes(s)
+    assert lib.efq_calibrate_workspace_bytes(ctypes.byref(s), 0) == 0
+
+    def cal(q=FAKE, oref=FAKE, t=T, nt=2, h=H, nh=2, b=ctypes.byref(best), ws=None, nbytes=0):
+        return lib.efq_calibrate(q, FAKE, FAKE, 0.125, 0, oref, ctypes.byref(s), t, nt, h, nh,
+                                 None, b, ws, nbytes, None)
+    assert cal(q=None) == L.EFQ_EINVAL
+    assert cal(oref=None) == L.EFQ_EINVAL
+    assert cal(b=None) == L.EFQ_EINVAL
+    assert cal(nt=0) == L.EFQ_EINVAL
+    bad = np.array([2.3, 0.0], np.float32)
+    assert cal(h=bad.ctypes.data_as(ctypes.c_void_p)) == L.EFQ_EINVAL
+    assert cal(ws=FAKE, nbytes=need - 1) == L.EFQ_EWORKSPACE
+
+
 def test_valid_call_without_gpu_reports_hip_error(L):
     import torch
     if torch.cuda.is_available():

@@ -219,3 +219,41 @@ def test_same_operand_v_constant(B):
         for kind in ("efq", "expq", "lut", "expq6"):
             out = B.attn_fwd(q.cuda(), k.cuda(), vc.cuda(), w.scale, True, kind)
             assert float((out - c).abs().max()) <= 1e-6 * abs(c) * 8
+
+
+def _bshd(rows_out, Bt, Hq, S, D):
+    """Oracle rows in (b, hq, i) order -> fp32 BSHD tensor."""
+    return torch.from_numpy(rows_out.reshape(Bt, Hq, S, D).transpose(0, 2, 1, 3).copy())
+
+
+def test_calibrate_matches_oracle(B, orc):
+    """Alg. 3 on the GPU against the oracle's Alg. 3, on exact-score inputs
+    with the exact-softmax reference: same objective grid (within fp32
+    accumulation order), and the selected pair is a minimiser of the
+    oracle's grid."""
+    w = inputs.Workload("cal", 1, 2, 1, 256, 64, False, "dyadic", 77)
+    q, k, v = inputs.dyadic_qkv(w)
+    qb, kb, vb = orc.bf16_bits(q), orc.bf16_bits(k), orc.bf16_bits(v)
+    ref = orc.attn(qb, kb, vb, w.scale, False, orc.EXACT)
+    o_ref = _bshd(ref, 1, 2, 256, 64).cuda()
+    taus, hs = [-3.5, -3.06, -2.6, -2.1], [1.9, 2.3, 2.8]
+    (tg, hg), rho_g = B.calibrate(q.cuda(), k.cuda(), v.cuda(), o_ref, taus, hs, w.scale, False)
+    (to, ho), rho_o = orc.calibrate(qb, kb, vb, w.scale, False, ref, taus, hs)
+    assert np.allclose(rho_g, rho_o, rtol=1e-4, atol=0)
+    i = [float(np.float32(t)) for t in taus].index(tg)
+    j = [float(np.float32(x)) for x in hs].index(hg)
+    assert rho_o[i, j] <= rho_o.min() * (1 + 1e-4)
+
+
+def test_calibrate_recovers_generating_point(B):
+    """With the GPU's own EFQ output at one candidate as the reference, that
+    candidate has rho = 0 (the same kernel on the same inputs) and is
+    selected."""
+    w = inputs.WORKLOADS["tiny"]
+    q, k, v = (t.cuda() for t in inputs.make_qkv(w))
+    taus, hs = [-3.5, -3.06, -2.6], [1.9, 2.3, 2.8]
+    o_ref = B.attn_fwd(q, k, v, w.scale, False, "efq", (-2.6, 1.9))
+    (tg, hg), rho = B.calibrate(q, k, v, o_ref, taus, hs, w.scale, False)
+    assert (tg, hg) == (float(np.float32(-2.6)), float(np.float32(1.9)))
+    assert rho[2, 0] == 0.0 and np.sum(rho == 0.0) == 1
+

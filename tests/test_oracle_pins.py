@@ -531,3 +531,39 @@ def test_rescaling_keeps_tiles_consistent(orc, dist):
         o512 = orc.attn(qb, kb, vb, w.scale, True, mode, bc=512)
         assert rho(o64, o512) < 0.12
     assert rho(orc.attn(qb, kb, vb, w.scale, True, orc.EXPQ, bc=64), ex) < 0.25
+
+
+# ------------------------------------------------------------ calibration
+def test_calibration_recovers_generating_point(orc):
+    """Alg. 3 pinned on a case with a known answer: when the reference
+    output is itself the EFQ output at one candidate pair, that pair has
+    rho = 0, every other pair on this input has rho > 0, and the search
+    returns it wherever it sits in the grid."""
+    w, q, k, v = _tiny(S=128, causal=False, Hq=2, Hkv=1)
+    qb, kb, vb = orc.bf16_bits(q), orc.bf16_bits(k), orc.bf16_bits(v)
+    taus, hs = [-3.5, -3.06, -2.6], [1.9, 2.3, 2.8]
+    for tau0, h0 in [(-3.06, 2.3), (-2.6, 1.9), (-3.5, 2.8)]:
+        ref = orc.attn(qb, kb, vb, w.scale, False, orc.EFQ, tau=tau0, h=h0)
+        best, rho = orc.calibrate(qb, kb, vb, w.scale, False, ref, taus, hs)
+        i, j = taus.index(tau0), hs.index(h0)
+        assert rho[i, j] == 0.0
+        assert np.sum(rho == 0.0) == 1
+        assert best == (float(np.float32(tau0)), float(np.float32(h0)))
+
+
+def test_calibration_objective_and_order(orc):
+    """rho is the relative Frobenius error of Sec. III-C and the selection
+    keeps the first strict minimum in tau-major order."""
+    w, q, k, v = _tiny(S=96, causal=True, Hq=1, Hkv=1)
+    qb, kb, vb = orc.bf16_bits(q), orc.bf16_bits(k), orc.bf16_bits(v)
+    ref = orc.attn(qb, kb, vb, w.scale, True, orc.EXACT)
+    taus, hs = [-3.3, -3.06, -3.06], [2.3, 2.3]      # repeated pairs tie exactly
+    best, rho = orc.calibrate(qb, kb, vb, w.scale, True, ref, taus, hs)
+    o = orc.attn(qb, kb, vb, w.scale, True, orc.EFQ, tau=-3.06, h=2.3)
+    want = np.linalg.norm(o.astype(np.float64) - ref) / np.linalg.norm(ref.astype(np.float64))
+    assert abs(rho[1, 0] - want) <= 1e-12 * want
+    assert rho[1, 0] == rho[1, 1] == rho[2, 0] == rho[2, 1]
+    flat = rho.ravel()
+    first = int(np.argmin(flat))                     # first occurrence of the minimum
+    assert best == (float(np.float32(taus[first // 2])), float(np.float32(hs[first % 2])))
+    assert np.all(rho > 0)
