@@ -73,6 +73,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU oracle time")
     ap.add_argument("--target-workload", default="qwen3_8b_32k",
                     help="second workload reported beside the headline one ('' to skip)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="sequence sweep of the Qwen3-8B heads (16K..128K, causal): fused-kernel "
+                         "time per probability stage, one JSON line per length")
     ap.add_argument("--pmc-run", action="store_true",
                     help="counter-collection run: the attention kernel 3 times, then a plain "
                          "device copy of COPY_BYTES bytes 3 times (the HBM-counter scale)")
@@ -90,6 +93,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     binding.lib()
     dev = torch.device("cuda:0")
+    if args.sweep:
+        sweep(args, binding, inputs, dev)
+        return
     w = inputs.WORKLOADS[args.workload]
     log(f"[bench] workload {w}")
     t0 = time.time()
@@ -240,6 +246,45 @@ def main():
         result["cpu_baseline"] = cpu_baseline(w, q, k, v, args.cpu_seconds)
 
     print(json.dumps(result), flush=True)
+
+
+def sweep(args, binding, inputs, dev):
+    """Fused-kernel time on the Qwen3-8B heads (32 q / 8 kv, D 128, causal)
+    over the sequence lengths of the paper's kernel table (16K..128K), for
+    each probability stage; the exposed stage cost is t(policy) - t(no-op).
+    One JSON line per length."""
+    import torch
+    base = inputs.WORKLOADS["qwen3_8b_32k"]
+    stream = torch.cuda.current_stream()
+    peak = 1.0 / (0.5 / PEAK_BF16 + 0.5 / PEAK_FP4)
+    for seq in (16384, 24576, 32768, 49152, 65536, 131072):
+        w = base.with_seq(seq)
+        q, k, v = inputs.make_qkv(w, device=dev)
+        vh = binding.quant_v(v, seq_q=w.seq, heads_q=w.heads_q, stream=stream)
+        out = torch.empty(q.shape, dtype=torch.float32, device=dev)
+        n = 10 if seq <= 32768 else 4
+        res = {"seq": seq, "causal": True, "pairs": w.pairs(), "flops": w.flops()}
+        for kind in ("efq", "expq", "expq6", "lut", "noop"):
+            prm = binding.PARAMS_LUT if kind == "lut" else binding.PARAMS_MEAN
+            for _ in range(3):   # warm-up
+                binding.attn_fwd_vhat(q, k, vh, w.scale, True, kind, prm, out=out, stream=stream)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(n):
+                binding.attn_fwd_vhat(q, k, vh, w.scale, True, kind, prm, out=out, stream=stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / n
+            tf = w.flops() / (ms * 1e-3) / 1e12
+            res[kind] = {"attn_ms": round(ms, 4), "tflops": round(tf, 1), "frac": round(tf / peak, 4)}
+        noop = res["noop"]["attn_ms"]
+        ex = {kd: res[kd]["attn_ms"] - noop for kd in ("efq", "expq", "expq6", "lut")}
+        res["exposed_ms"] = {kd: round(x, 4) for kd, x in ex.items()}
+        res["exposed_speedup_vs_expq"] = round(1 - ex["efq"] / ex["expq"], 4) if ex["expq"] > 0 else None
+        print(json.dumps(res), flush=True)
+        del q, k, v, vh, out
+        torch.cuda.empty_cache()
 
 
 def target_run(args, binding, inputs, dev, stream):
