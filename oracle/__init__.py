@@ -65,8 +65,9 @@ def lib():
         L.orc_quant_v.argtypes = [P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, P, P]
         L.orc_attn.argtypes = [P, P, P] + [ctypes.c_int] * 6 + [
             ctypes.c_float, ctypes.c_int, ctypes.c_int, ctypes.c_float, ctypes.c_float,
-            ctypes.c_int, P, ctypes.c_long, P, P, P, P, P, P, ctypes.c_int]
-        for f in (L.orc_pgen, L.orc_pgen_real, L.orc_quant_v, L.orc_attn):
+            ctypes.c_int, P, ctypes.c_long, P, P, P, P, P, P, ctypes.c_int, ctypes.c_int]
+        L.orc_quant_mxfp8.argtypes = [P, ctypes.c_long, ctypes.c_int, P, P]
+        for f in (L.orc_pgen, L.orc_pgen_real, L.orc_quant_v, L.orc_attn, L.orc_quant_mxfp8):
             f.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -139,14 +140,15 @@ def all_rows(B: int, Hq: int, Sq: int) -> np.ndarray:
 
 def attn(q_bits, k_bits, v_bits, scale: float, causal: bool, mode: int = EFQ,
          tau: float = None, h: float = None, bc: int = 64, rows: np.ndarray = None,
-         dump: bool = False, nthreads: int = 0, margins: bool = False):
+         dump: bool = False, nthreads: int = 0, margins: bool = False, qk8: bool = False):
     """Attention forward for the listed query rows (Alg. 2 over tiles of bc keys).
 
     q_bits [B, Sq, Hq, D], k_bits/v_bits [B, Sk, Hkv, D]: bf16 bit patterns.
     rows: int32 [n, 3] of (b, hq, i); None = every row, ordered (b, hq, i).
     Returns out [n, D] fp32, plus (codes [n, nblk*32], e8m0 [n, nblk],
     m [n] fp32, l [n] fp64) when dump is set, plus the per-row smallest
-    decision margin [n] fp64 (in dot-product units) when margins is set."""
+    decision margin [n] fp64 (in dot-product units) when margins is set.
+    qk8: Q K^T on the MXFP8 values of Q and K (low-bit Q K^T)."""
     q_bits = np.ascontiguousarray(q_bits, dtype=np.uint16)
     k_bits = np.ascontiguousarray(k_bits, dtype=np.uint16)
     v_bits = np.ascontiguousarray(v_bits, dtype=np.uint16)
@@ -169,7 +171,7 @@ def attn(q_bits, k_bits, v_bits, scale: float, causal: bool, mode: int = EFQ,
     rc = lib().orc_attn(_ptr(q_bits), _ptr(k_bits), _ptr(v_bits), B, Sq, Sk, Hq, Hkv, D,
                         float(scale), int(causal), int(mode), tau, h, int(bc), _ptr(rows), n,
                         _ptr(out), _ptr(codes), _ptr(e8), _ptr(mm), _ptr(ll), _ptr(mg),
-                        int(nthreads))
+                        int(bool(qk8)), int(nthreads))
     if rc != 0:
         raise ValueError(f"orc_attn failed with {rc}")
     res = (out,)
@@ -180,6 +182,30 @@ def attn(q_bits, k_bits, v_bits, scale: float, causal: bool, mode: int = EFQ,
     return res if len(res) > 1 else out
 
 
+
+
+def quant_mxfp8(x_bits: np.ndarray):
+    """MXFP8 (E4M3) along the last axis (a multiple of 32) of bf16 bits x:
+    returns (codes uint8 [..., D], e8m0 uint8 [..., D/32])."""
+    x_bits = np.ascontiguousarray(x_bits, dtype=np.uint16)
+    D = x_bits.shape[-1]
+    rows = x_bits.size // D
+    codes = np.zeros(x_bits.shape, np.uint8)
+    e8 = np.zeros(x_bits.shape[:-1] + (D // 32,), np.uint8)
+    rc = lib().orc_quant_mxfp8(_ptr(x_bits), rows, D, _ptr(codes), _ptr(e8))
+    if rc != 0:
+        raise ValueError(f"orc_quant_mxfp8 failed with {rc}")
+    return codes, e8
+
+
+def e4m3_values(codes: np.ndarray, e8m0: np.ndarray) -> np.ndarray:
+    """fp64 values of MXFP8 codes with their per-32 E8M0 scales."""
+    c = codes.astype(np.int64)
+    e = (c >> 3) & 15
+    m = c & 7
+    mag = np.where(e == 0, m * 2.0 ** -9, (1 + m / 8.0) * 2.0 ** (e - 7.0))
+    k = np.repeat(e8m0.astype(np.int64) - 127, 32, axis=-1)
+    return np.where(c & 0x80, -1.0, 1.0) * mag * 2.0 ** k
 
 def calibrate(q_bits, k_bits, v_bits, scale: float, causal: bool, o_ref: np.ndarray, taus, hs,
               bc: int = 64, nthreads: int = 0):

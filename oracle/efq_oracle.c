@@ -20,6 +20,12 @@
  *     the table C16 of Sec. II-D (EFQ-Softmax-LUT).
  *   - Exp-then-quantize baseline (pgen_block_expq): Eq. (post-softmax-path):
  *     FP32 probabilities exp(x), then the OCP MXFP4 quantiser.
+ *   - Low-bit Q K^T (orc_quant_mxfp8, orc_attn with qk8 set): the paper
+ *     frames low-bit attention as running Q K^T (and P V) on FP8/FP4 matrix
+ *     engines (Sec. I).  Q and K are then MXFP8 under the OCP microscaling
+ *     rule: per 32 consecutive elements along head_dim, shared exponent
+ *     floor(log2 amax) - 8 (8 = largest E4M3 exponent), E4M3 elements
+ *     rounded to nearest (ties to even), saturating at 448.
  *   - The online recurrence (orc_attn): Algorithm 2 for every key/value tile
  *     in ascending order: Eqs. (rowmax-update), (alpha), (numerator-basic),
  *     (denominator-basic) and the final division of Sec. III-A.
@@ -402,6 +408,93 @@ static double e2m1_value(uint8_t c, int k)
     return (c & 8u) ? -v : v;
 }
 
+/* Magnitude of the E4M3 code c (0 <= c < 0x7F, sign bit clear): exponent
+ * field e (bias 7), mantissa m; e = 0 is subnormal, m * 2^-9.  0x7F is NaN
+ * and is never produced. */
+static double e4m3_magnitude(int c)
+{
+    int e = (c >> 3) & 15, m = c & 7;
+    return e == 0 ? ldexp((double)m, -9) : ldexp(1.0 + m / 8.0, e - 7);
+}
+
+/* Nearest E4M3 magnitude code for y >= 0, ties to the even code (even
+ * mantissa bit), values above 448 saturate to 448 (code 0x7E).  A search
+ * over all 127 finite non-negative codes, which increase with the code. */
+static int e4m3_nearest(double y)
+{
+    int best = 0;
+    double bd = fabs(y - e4m3_magnitude(0));
+    for (int c = 1; c < 0x7F; ++c) {
+        double d = fabs(y - e4m3_magnitude(c));
+        if (d < bd || (d == bd && (c % 2) == 0 && (best % 2) != 0)) {
+            best = c;
+            bd = d;
+        }
+    }
+    return best;
+}
+
+/* ------------------------------------------------------------------------
+ * MXFP8 (E4M3) quantiser for Q and K: x is rows x D bf16 bits (D a multiple
+ * of 32); for each row and 32-element block: k = floor(log2 amax) - 8
+ * clamped to [-127, 127] (amax = 0: k = -127), codes = sign | nearest
+ * E4M3 of |x| 2^-k.  codes: rows x D bytes, e8m0: rows x D/32 bytes (k+127).
+ * ---------------------------------------------------------------------- */
+int orc_quant_mxfp8(const uint16_t *x, long rows, int D, uint8_t *codes, uint8_t *e8m0)
+{
+    if (!x || !codes || !e8m0 || rows < 0 || D < 32 || D % 32 != 0)
+        return -1;
+    for (long r = 0; r < rows; ++r)
+        for (int blk = 0; blk < D / 32; ++blk) {
+            const uint16_t *xb = x + r * D + blk * 32;
+            double amax = 0.0;
+            for (int t = 0; t < 32; ++t) {
+                double a = fabs((double)bf16_to_f32(xb[t]));
+                if (a > amax)
+                    amax = a;
+            }
+            int k = K_MIN;
+            if (amax > 0.0)
+                k = clampi(floor_log2(amax) - 8, K_MIN, K_MAX);
+            e8m0[r * (D / 32) + blk] = (uint8_t)(k + 127);
+            for (int t = 0; t < 32; ++t) {
+                double y = fabs((double)bf16_to_f32(xb[t]));
+                int c = e4m3_nearest(ldexp(y, -k));
+                if (xb[t] & 0x8000u)
+                    c |= 0x80;
+                codes[r * D + blk * 32 + t] = (uint8_t)c;
+            }
+        }
+    return 0;
+}
+
+/* value of an MXFP8 element: E4M3 code (bit 7 = sign) times 2^k */
+static double e4m3_value(uint8_t c, int k)
+{
+    double v = ldexp(e4m3_magnitude(c & 0x7F), k);
+    return (c & 0x80u) ? -v : v;
+}
+
+/* Q or K as the values the low-bit Q K^T multiplies: [rows][D] doubles. */
+static double *mxfp8_values(const uint16_t *x, long rows, int D)
+{
+    uint8_t *c = malloc((size_t)rows * D);
+    uint8_t *e = malloc((size_t)rows * (D / 32));
+    double *out = malloc(sizeof(double) * (size_t)rows * D);
+    if (!c || !e || !out || orc_quant_mxfp8(x, rows, D, c, e) != 0) {
+        free(c);
+        free(e);
+        free(out);
+        return NULL;
+    }
+    for (long r = 0; r < rows; ++r)
+        for (int d = 0; d < D; ++d)
+            out[r * D + d] = e4m3_value(c[r * D + d], (int)e[r * (D / 32) + d / 32] - 127);
+    free(c);
+    free(e);
+    return out;
+}
+
 /* ---------------------------------------------------------------------- *
  * Attention forward for a list of query rows, Algorithm 2 over key/value
  * tiles of width bc (a multiple of 32) in ascending key order.
@@ -423,7 +516,7 @@ int orc_attn(const uint16_t *q, const uint16_t *kmat, const uint16_t *v, int B, 
              int Sk, int Hq, int Hkv, int D, float scale, int causal, int mode, float tau,
              float h, int bc, const int32_t *rows, long nrows, float *out,
              uint8_t *dump_codes, uint8_t *dump_e8m0, float *dump_m, double *dump_l,
-             double *row_margin, int nthreads)
+             double *row_margin, int qk8, int nthreads)
 {
     if (!q || !kmat || !v || !rows || !out || B < 1 || Sq < 1 || Sk < 1 || Hq < 1 ||
         Hkv < 1 || D < 1 || Hq % Hkv != 0 || bc < 32 || bc % 32 != 0 || bc > 1024)
@@ -433,6 +526,19 @@ int orc_attn(const uint16_t *q, const uint16_t *kmat, const uint16_t *v, int B, 
     const int nblk = (Sk + 31) / 32;
     const int group = Hq / Hkv;
     const int quant = (mode != ORC_EXACT);
+    if (qk8 && D % 32 != 0)
+        return -1;
+    /* low-bit Q K^T: Q and K as their MXFP8 values */
+    double *q8 = NULL, *k8 = NULL;
+    if (qk8) {
+        q8 = mxfp8_values(q, (long)B * Sq * Hq, D);
+        k8 = mxfp8_values(kmat, (long)B * Sk * Hkv, D);
+        if (!q8 || !k8) {
+            free(q8);
+            free(k8);
+            return -2;
+        }
+    }
 
     /* Quantised V for every (b, kv head): [B][Hkv][nblk*32][D] values. */
     double *vhat = NULL;
@@ -484,8 +590,10 @@ int orc_attn(const uint16_t *q, const uint16_t *kmat, const uint16_t *v, int B, 
             free(acc); free(cd); free(A); free(dA); free(qd);
             continue;
         }
-        for (int d = 0; d < D; ++d)
-            qd[d] = bf16_to_f32(q[(((long)b * Sq + i) * Hq + hq) * D + d]);
+        for (int d = 0; d < D; ++d) {
+            long qi = (((long)b * Sq + i) * Hq + hq) * D + d;
+            qd[d] = qk8 ? q8[qi] : (double)bf16_to_f32(q[qi]);
+        }
         /* blocks that are never processed (past the causal limit) read as
          * fully masked blocks: codes 0 and E8M0 0x00 */
         if (dump_codes)
@@ -511,10 +619,10 @@ int orc_attn(const uint16_t *q, const uint16_t *kmat, const uint16_t *v, int B, 
                     dots[t] = -INFINITY;
                     continue;
                 }
-                const uint16_t *kr = kmat + (((long)b * Sk + key) * Hkv + g) * D;
+                const long kb0 = (((long)b * Sk + key) * Hkv + g) * D;
                 double s = 0.0;
                 for (int d = 0; d < D; ++d)
-                    s += qd[d] * (double)bf16_to_f32(kr[d]);
+                    s += qd[d] * (qk8 ? k8[kb0 + d] : (double)bf16_to_f32(kmat[kb0 + d]));
                 acc[t] = (float)s;
                 dots[t] = s;
             }
@@ -602,8 +710,10 @@ int orc_attn(const uint16_t *q, const uint16_t *kmat, const uint16_t *v, int B, 
         free(acc); free(cd); free(A); free(dA); free(qd);
     }
     free(vhat);
+    free(q8);
+    free(k8);
     return fail ? -1 : 0;
 }
 
 /* Version tag so the Python side can tell a stale build. */
-int orc_version(void) { return 2; }
+int orc_version(void) { return 3; }

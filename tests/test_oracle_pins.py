@@ -567,3 +567,109 @@ def test_calibration_objective_and_order(orc):
     first = int(np.argmin(flat))                     # first occurrence of the minimum
     assert best == (float(np.float32(taus[first // 2])), float(np.float32(hs[first % 2])))
     assert np.all(rho > 0)
+
+
+# ------------------------------------------------------- MXFP8 Q / K (low-bit Q K^T)
+def _e4m3_bits_torch(y):
+    """torch's own float32 -> float8_e4m3fn cast (round to nearest even)."""
+    return torch.from_numpy(np.ascontiguousarray(y, np.float32)).to(torch.float8_e4m3fn) \
+        .view(torch.uint8).numpy()
+
+
+def _mxfp8_dequant_torch(codes, e8):
+    """Values of MXFP8 codes decoded by torch's float8_e4m3fn type."""
+    v = torch.from_numpy(np.ascontiguousarray(codes)).view(torch.float8_e4m3fn).double().numpy()
+    return v * np.repeat(2.0 ** (e8.astype(np.float64) - 127), 32, axis=-1)
+
+
+def test_mxfp8_scale_rule(orc):
+    """OCP microscaling for E4M3: the shared exponent is floor(log2 amax)
+    minus 8 (the largest E4M3 exponent), written as E8M0 (k + 127); an
+    all-zero block takes the smallest scale."""
+    rng = np.random.default_rng(20)
+    x = (rng.standard_normal((4000, 64)) * 2.0 ** rng.integers(-30, 30, (4000, 1))).astype(np.float32)
+    x[5, :32] = 0.0
+    xb = orc_bits(torch.from_numpy(x))
+    codes, e8 = orc.quant_mxfp8(xb)
+    xv = orc.bits_to_f64(xb).reshape(4000, 2, 32)
+    amax = np.abs(xv).max(axis=2)
+    expo = np.array([[math.frexp(a)[1] - 1 if a > 0 else -119 for a in r] for r in amax])
+    want = np.clip(expo - 8, -127, 127) + 127
+    want[5, 0] = 0
+    assert np.array_equal(e8.astype(np.int64), want)
+    assert np.all(codes[5, :32] == 0)
+
+
+def test_mxfp8_codes_match_torch_cast(orc):
+    """Element codes are the round-to-nearest-even E4M3 of x / 2^k, which
+    is torch's float8_e4m3fn cast wherever |x| / 2^k <= 464 (torch turns
+    larger values into NaN); above that the MX rule saturates to 448
+    (code 0x7E with the sign)."""
+    rng = np.random.default_rng(21)
+    w = inputs.Workload("t", 1, 4, 2, 512, 128, False, "qwen", 21)
+    q, k, _ = inputs.make_qkv(w)
+    for t in (q, k, torch.from_numpy(rng.standard_normal((300, 96)).astype(np.float32) * 3)):
+        xb = orc_bits(t)
+        D = xb.shape[-1]
+        codes, e8 = orc.quant_mxfp8(xb)
+        xv = orc.bits_to_f64(xb).reshape(-1, D)
+        sc = np.repeat(2.0 ** (e8.reshape(-1, D // 32).astype(np.float64) - 127), 32, axis=1)
+        y = xv / sc
+        assert np.all(np.abs(y) < 512)                 # amax / 2^k < 2^9
+        ref = _e4m3_bits_torch(y)
+        big = np.abs(y) > 464
+        got = codes.reshape(-1, D)
+        assert np.array_equal(got[~big], ref[~big])
+        assert np.all((got[big] & 0x7F) == 0x7E)
+        assert np.array_equal(got[big] >> 7, (y[big] < 0).astype(np.uint8))
+
+
+def test_mxfp8_grid_round_trip_ties_and_saturation(orc):
+    """Every finite E4M3 value times a power of two comes back unchanged in
+    a block whose maximum is 448 * 2^j; midpoints go to the even mantissa;
+    460 saturates to 448 and 2^-10 (half the smallest subnormal) to zero."""
+    mags = np.array([torch.tensor([c], dtype=torch.uint8).view(torch.float8_e4m3fn).double().item()
+                     for c in range(0x7F)])
+    vals = np.concatenate([mags, -mags[1:]])           # 253 codes
+    rows = []
+    for j in (-12, 0, 7):
+        for s in range(0, len(vals), 31):
+            blk = np.zeros(32)
+            blk[0] = 448.0
+            part = vals[s:s + 31]
+            blk[1:1 + len(part)] = part
+            rows.append(blk * 2.0 ** j)
+    x = np.array(rows)
+    codes, e8 = orc.quant_mxfp8(orc_bits(torch.from_numpy(x)))
+    back = _mxfp8_dequant_torch(codes, e8)
+    assert np.array_equal(back, x)
+    # ties and saturation in a block with k = 0
+    blk = np.zeros((1, 32))
+    blk[0, :7] = [448.0, 1.0625, 1.1875, 460.0, -460.0, 2.0 ** -10, 3 * 2.0 ** -11]
+    codes, e8 = orc.quant_mxfp8(orc_bits(torch.from_numpy(blk)))
+    assert e8[0, 0] == 127
+    assert list(codes[0, :7]) == [0x7E, 0x38, 0x3A, 0x7E, 0xFE, 0x00, 0x01]
+
+
+def test_lowbit_attention_is_attention_on_mxfp8_values(orc):
+    """With qk8 set, the recurrence runs on the MXFP8 values of Q and K:
+    the same output as the plain path on those values (decoded by torch and
+    exactly representable in bf16), for every P mode; and inputs already on
+    the MXFP8 grid are left unchanged by it."""
+    w, q, k, v = _tiny(S=160, D=64, Hq=4, Hkv=2, dist="qwen", causal=True)
+    qb, kb, vb = orc.bf16_bits(q), orc.bf16_bits(k), orc.bf16_bits(v)
+    deq = []
+    for xb in (qb, kb):
+        c, e = orc.quant_mxfp8(xb)
+        d = _mxfp8_dequant_torch(c, e)
+        db = orc_bits(torch.from_numpy(d))
+        assert np.array_equal(orc.bits_to_f64(db), d)      # exact in bf16
+        deq.append(db)
+    for mode in (orc.EFQ, orc.EXPQ, orc.EXACT):
+        a = orc.attn(qb, kb, vb, w.scale, True, mode, bc=64, qk8=True)
+        b = orc.attn(deq[0], deq[1], vb, w.scale, True, mode, bc=64)
+        c = orc.attn(deq[0], deq[1], vb, w.scale, True, mode, bc=64, qk8=True)
+        assert np.array_equal(a, b) and np.array_equal(b, c)
+    # and it is a different (lower precision) computation from the bf16 path
+    assert not np.array_equal(orc.attn(qb, kb, vb, w.scale, True, orc.EXACT, bc=64),
+                              orc.attn(qb, kb, vb, w.scale, True, orc.EXACT, bc=64, qk8=True))
