@@ -140,6 +140,55 @@ int efq_attn_fwd_expq(const void *q, const void *k, const void *v, float scale, 
                       float *out, const efq_shape *s, efq_stream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * Low-bit Q K^T.  The paper places EFQ inside low-bit attention, whose Q K^T
+ * also runs on FP8 matrix engines (Sec. I).  Here Q and K are MXFP8 under
+ * the OCP microscaling rule: per row and 32 consecutive head-dim elements
+ * an E8M0 exponent k = floor(log2 amax) - 8 (8 = the largest E4M3 exponent;
+ * k = -127 for a block whose amax is 0 or below the normal bf16 range),
+ * elements E4M3 (OCP E4M3FN, bias 7) of |x| 2^-k rounded to nearest even
+ * and saturating at 448, sign bit = sign of the bf16 input.  S = Q K^T then
+ * runs on the block-scaled FP8 matrix core; everything after the scores is
+ * as in efq_attn_fwd_vhat.
+ *
+ * Q^ layout, with sq_pad = 64 * ceil(seq_q / 64) (rows past seq_q are zero):
+ *   codes  [batch][heads_q][sq_pad][head_dim]      E4M3 bytes
+ *   scales [batch][heads_q][sq_pad][head_dim/32]   E8M0 bytes, starting at
+ *                                                  efq_qhat_scale_offset(s)
+ * K^ likewise with heads_kv, seq_k and efq_khat_scale_offset(s).
+ * ------------------------------------------------------------------------- */
+size_t efq_qhat_bytes(const efq_shape *s);
+size_t efq_qhat_scale_offset(const efq_shape *s);
+size_t efq_khat_bytes(const efq_shape *s);
+size_t efq_khat_scale_offset(const efq_shape *s);
+
+/* Q, K (bf16 BSHD, device) -> Q^ and K^ (device buffers of at least
+ * efq_qhat_bytes(s) and efq_khat_bytes(s) bytes). */
+int efq_quant_qk_mxfp8(const void *q, const void *k, const efq_shape *s, void *qhat,
+                       size_t qhat_bytes, void *khat, size_t khat_bytes, efq_stream_t stream);
+
+/* Attention forward on Q^, K^ (efq_quant_qk_mxfp8) and V~ (efq_quant_v_mxfp4)
+ * of the same shape; kind, p, scale and out as in efq_attn_fwd_vhat. */
+int efq_attn_fwd_qk8(const void *qhat, size_t qhat_bytes, const void *khat, size_t khat_bytes,
+                     const void *vhat, size_t vhat_bytes, float scale, int causal, int kind,
+                     efq_params p, float *out, const efq_shape *s, efq_stream_t stream);
+
+/* efq_attn_fwd_qk8 recording the probability stage, as efq_attn_fwd_dump. */
+int efq_attn_fwd_qk8_dump(const void *qhat, size_t qhat_bytes, const void *khat,
+                          size_t khat_bytes, const void *vhat, size_t vhat_bytes, float scale,
+                          int causal, int kind, efq_params p, float *out, const efq_shape *s,
+                          uint8_t *p_codes, uint8_t *p_e8m0, float *row_m, float *row_l,
+                          efq_stream_t stream);
+
+/* All three quantisers and the attention with one workspace of at least
+ * efq_attn_lowbit_workspace_bytes(s) bytes, 256-byte aligned (Q^, K^ and V~
+ * at 256-byte boundaries in that order); ws may be NULL with ws_bytes == 0
+ * (one stream-ordered allocation, released on the same stream). */
+size_t efq_attn_lowbit_workspace_bytes(const efq_shape *s);
+int efq_attn_fwd_lowbit_ex(const void *q, const void *k, const void *v, float scale, int causal,
+                           int kind, efq_params p, float *out, const efq_shape *s, void *ws,
+                           size_t ws_bytes, efq_stream_t stream);
+
+/* ---------------------------------------------------------------------------
  * Offline selection of (tau, h), Algorithm 3 and Sec. III-C: for every
  * candidate pair (taus[i], hs[j]), i outer and j inner, run the EFQ attention
  * forward on the calibration inputs and compute

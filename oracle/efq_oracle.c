@@ -418,20 +418,28 @@ static double e4m3_magnitude(int c)
 }
 
 /* Nearest E4M3 magnitude code for y >= 0, ties to the even code (even
- * mantissa bit), values above 448 saturate to 448 (code 0x7E).  A search
- * over all 127 finite non-negative codes, which increase with the code. */
+ * mantissa bit), values above 448 saturate to 448 (code 0x7E).  The 127
+ * finite non-negative codes increase with their magnitude: bisect for the
+ * last code c whose magnitude is <= y, then take c or c + 1, whichever is
+ * nearer. */
 static int e4m3_nearest(double y)
 {
-    int best = 0;
-    double bd = fabs(y - e4m3_magnitude(0));
-    for (int c = 1; c < 0x7F; ++c) {
-        double d = fabs(y - e4m3_magnitude(c));
-        if (d < bd || (d == bd && (c % 2) == 0 && (best % 2) != 0)) {
-            best = c;
-            bd = d;
-        }
+    if (y >= e4m3_magnitude(0x7E))
+        return 0x7E;
+    int lo = 0, hi = 0x7E; /* magnitude(lo) <= y < magnitude(hi) */
+    while (hi - lo > 1) {
+        int mid = (lo + hi) / 2;
+        if (e4m3_magnitude(mid) <= y)
+            lo = mid;
+        else
+            hi = mid;
     }
-    return best;
+    double dl = y - e4m3_magnitude(lo), dh = e4m3_magnitude(hi) - y;
+    if (dl < dh)
+        return lo;
+    if (dh < dl)
+        return hi;
+    return (lo % 2 == 0) ? lo : hi;
 }
 
 /* ------------------------------------------------------------------------
@@ -528,16 +536,13 @@ int orc_attn(const uint16_t *q, const uint16_t *kmat, const uint16_t *v, int B, 
     const int quant = (mode != ORC_EXACT);
     if (qk8 && D % 32 != 0)
         return -1;
-    /* low-bit Q K^T: Q and K as their MXFP8 values */
-    double *q8 = NULL, *k8 = NULL;
+    /* low-bit Q K^T: K as its MXFP8 values (each Q row is quantised when
+     * its row is processed) */
+    double *k8 = NULL;
     if (qk8) {
-        q8 = mxfp8_values(q, (long)B * Sq * Hq, D);
         k8 = mxfp8_values(kmat, (long)B * Sk * Hkv, D);
-        if (!q8 || !k8) {
-            free(q8);
-            free(k8);
+        if (!k8)
             return -2;
-        }
     }
 
     /* Quantised V for every (b, kv head): [B][Hkv][nblk*32][D] values. */
@@ -590,10 +595,16 @@ int orc_attn(const uint16_t *q, const uint16_t *kmat, const uint16_t *v, int B, 
             free(acc); free(cd); free(A); free(dA); free(qd);
             continue;
         }
-        for (int d = 0; d < D; ++d) {
-            long qi = (((long)b * Sq + i) * Hq + hq) * D + d;
-            qd[d] = qk8 ? q8[qi] : (double)bf16_to_f32(q[qi]);
+        const long q0 = (((long)b * Sq + i) * Hq + hq) * D;
+        double *qrow8 = qk8 ? mxfp8_values(q + q0, 1, D) : NULL;
+        if (qk8 && !qrow8) {
+            fail = 1;
+            free(acc); free(cd); free(A); free(dA); free(qd);
+            continue;
         }
+        for (int d = 0; d < D; ++d)
+            qd[d] = qk8 ? qrow8[d] : (double)bf16_to_f32(q[q0 + d]);
+        free(qrow8);
         /* blocks that are never processed (past the causal limit) read as
          * fully masked blocks: codes 0 and E8M0 0x00 */
         if (dump_codes)
@@ -710,7 +721,6 @@ int orc_attn(const uint16_t *q, const uint16_t *kmat, const uint16_t *v, int B, 
         free(acc); free(cd); free(A); free(dA); free(qd);
     }
     free(vhat);
-    free(q8);
     free(k8);
     return fail ? -1 : 0;
 }

@@ -67,6 +67,15 @@ SIGNATURES = {
     "efq_pgen_bench": ([I, Params, I, I, P, P], I),
     "efq_calibrate_workspace_bytes": ([SP, I], SZ),
     "efq_calibrate": ([P, P, P, F, I, P, SP, P, I, P, I, P, ctypes.POINTER(Params), P, SZ, P], I),
+    "efq_qhat_bytes": ([SP], SZ),
+    "efq_qhat_scale_offset": ([SP], SZ),
+    "efq_khat_bytes": ([SP], SZ),
+    "efq_khat_scale_offset": ([SP], SZ),
+    "efq_quant_qk_mxfp8": ([P, P, SP, P, SZ, P, SZ, P], I),
+    "efq_attn_fwd_qk8": ([P, SZ, P, SZ, P, SZ, F, I, I, Params, P, SP, P], I),
+    "efq_attn_fwd_qk8_dump": ([P, SZ, P, SZ, P, SZ, F, I, I, Params, P, SP, P, P, P, P, P], I),
+    "efq_attn_lowbit_workspace_bytes": ([SP], SZ),
+    "efq_attn_fwd_lowbit_ex": ([P, P, P, F, I, I, Params, P, SP, P, SZ, P], I),
 }
 
 
@@ -221,6 +230,91 @@ def attn_fwd_dump(q, k, vhat, scale=None, causal=False, kind="efq", params=None,
                                    _ptr(row_l), _stream(stream)))
     return out, codes, e8, row_m, row_l
 
+
+
+def quant_qk(q, k, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Q, K (bf16 BSHD) -> the MXFP8 byte buffers Q^ and K^ (layout in efq_attn.h)."""
+    _bf16(q, "q")
+    _bf16(k, "k")
+    sh = shape_of(q, k)
+    qh = torch.empty(int(lib().efq_qhat_bytes(ctypes.byref(sh))), dtype=torch.uint8, device=q.device)
+    kh = torch.empty(int(lib().efq_khat_bytes(ctypes.byref(sh))), dtype=torch.uint8, device=q.device)
+    _check(lib().efq_quant_qk_mxfp8(_ptr(q), _ptr(k), ctypes.byref(sh), _ptr(qh), qh.numel(),
+                                    _ptr(kh), kh.numel(), _stream(stream)))
+    return qh, kh
+
+
+def attn_fwd_qk8(qhat, khat, vhat, shape: Shape, scale: Optional[float] = None,
+                 causal: bool = False, kind="efq", params=None, out: Optional[torch.Tensor] = None,
+                 stream=None) -> torch.Tensor:
+    """Attention on pre-quantised Q^, K^ (quant_qk) and V~ (quant_v); fp32 BSHD out."""
+    kind = _kind(kind)
+    if scale is None:
+        scale = shape.head_dim ** -0.5
+    if out is None:
+        out = torch.empty((shape.batch, shape.seq_q, shape.heads_q, shape.head_dim),
+                          dtype=torch.float32, device=qhat.device)
+    _check(lib().efq_attn_fwd_qk8(_ptr(qhat), qhat.numel(), _ptr(khat), khat.numel(), _ptr(vhat),
+                                  vhat.numel(), float(scale), int(causal), kind,
+                                  _params(kind, params), _ptr(out), ctypes.byref(shape),
+                                  _stream(stream)))
+    return out
+
+
+def attn_fwd_qk8_dump(qhat, khat, vhat, shape: Shape, scale=None, causal=False, kind="efq",
+                      params=None, stream=None):
+    """attn_fwd_qk8 plus the probability-stage record, as attn_fwd_dump."""
+    kind = _kind(kind)
+    scale = shape.head_dim ** -0.5 if scale is None else scale
+    B, Sq, Hq, D, Sk = shape.batch, shape.seq_q, shape.heads_q, shape.head_dim, shape.seq_k
+    nblk = (Sk + 31) // 32
+    dev = qhat.device
+    out = torch.empty((B, Sq, Hq, D), dtype=torch.float32, device=dev)
+    codes = torch.empty((B, Hq, Sq, nblk * 16), dtype=torch.uint8, device=dev)
+    e8 = torch.empty((B, Hq, Sq, nblk), dtype=torch.uint8, device=dev)
+    row_m = torch.empty((B, Hq, Sq), dtype=torch.float32, device=dev)
+    row_l = torch.empty((B, Hq, Sq), dtype=torch.float32, device=dev)
+    _check(lib().efq_attn_fwd_qk8_dump(_ptr(qhat), qhat.numel(), _ptr(khat), khat.numel(),
+                                       _ptr(vhat), vhat.numel(), float(scale), int(causal), kind,
+                                       _params(kind, params), _ptr(out), ctypes.byref(shape),
+                                       _ptr(codes), _ptr(e8), _ptr(row_m), _ptr(row_l),
+                                       _stream(stream)))
+    return out, codes, e8, row_m, row_l
+
+
+def attn_fwd_lowbit(q, k, v, scale: Optional[float] = None, causal: bool = False, kind="efq",
+                    params=None, out: Optional[torch.Tensor] = None,
+                    workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Low-bit attention: MXFP8 Q K^T, the chosen probability stage, MXFP4 P~V.
+    workspace: None, or a 256-byte aligned uint8 tensor of at least
+    lowbit_workspace_bytes(shape) bytes."""
+    _bf16(q, "q")
+    _bf16(k, "k")
+    _bf16(v, "v")
+    sh = shape_of(q, k)
+    kind = _kind(kind)
+    if scale is None:
+        scale = q.shape[-1] ** -0.5
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    ws_n = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().efq_attn_fwd_lowbit_ex(_ptr(q), _ptr(k), _ptr(v), float(scale), int(causal), kind,
+                                        _params(kind, params), _ptr(out), ctypes.byref(sh),
+                                        _ptr(workspace), ws_n, _stream(stream)))
+    return out
+
+
+def lowbit_workspace_bytes(shape: Shape) -> int:
+    return int(lib().efq_attn_lowbit_workspace_bytes(ctypes.byref(shape)))
+
+
+def qk8_natural(buf: torch.Tensor, batch: int, heads: int, seq: int, head_dim: int, scale_off: int):
+    """A Q^ or K^ buffer -> (codes [B, H, seq, D], e8m0 [B, H, seq, D/32]) without padding rows."""
+    sp = 64 * ((seq + 63) // 64)
+    n = batch * heads * sp
+    codes = buf[: n * head_dim].view(batch, heads, sp, head_dim)[:, :, :seq]
+    e8 = buf[scale_off: scale_off + n * (head_dim // 32)].view(batch, heads, sp, head_dim // 32)
+    return codes, e8[:, :, :seq]
 
 
 def calibrate(q, k, v, o_ref, taus, hs, scale: Optional[float] = None, causal: bool = False,

@@ -420,6 +420,59 @@ __global__ __launch_bounds__(256) void vquant_kernel(const unsigned short* __res
   }
 }
 
+// ------------------------------------------------ MXFP8 Q / K quantiser
+// Low-bit Q K^T: Q and K as MXFP8 under the OCP microscaling rule, per row
+// and 32 consecutive head-dim elements: E8M0 exponent k = floor(log2 amax)
+// - 8 (8 = the largest E4M3 exponent; amax = 0 or below the normal bf16
+// range: k = -127), elements E4M3 (bias 7) of |x| 2^-k rounded to nearest
+// even, saturating at 448, sign bit = sign of the bf16 input.  Output rows
+// are [batch][head][padded seq] (rows past seq are zero): codes [..][D],
+// scales [..][D/32] at soff.
+struct Q8Args {
+  int B, S, H, D, s_pad;
+  size_t soff;
+};
+
+// E4M3 code of |x| 2^-k for bf16 bits x, with |x| 2^-k < 512: the binade
+// exponent E of y (at least -6, the subnormal binade), the 3-bit mantissa
+// step 2^(E-3), y / step rounded to nearest even (a carry into the next
+// binade yields the right code), saturated to 448.
+__device__ __forceinline__ unsigned e4m3_code(unsigned bits, int k) {
+  const float y = ldexpf(__uint_as_float((bits & 0x7fffu) << 16), -k);
+  const int E = max((int)((__float_as_uint(y) >> 23) & 255u) - 127, -6);
+  const int q = (int)rintf(ldexpf(y, 3 - E));
+  const unsigned c = (unsigned)min(((E + 7) << 3) + q - 8, 0x7E);
+  return c | ((bits >> 8) & 0x80u);
+}
+
+// One thread per 8 elements (4 threads per 32-element block, lanes 4i..4i+3).
+__global__ __launch_bounds__(256) void mxfp8_kernel(const unsigned short* __restrict__ x,
+                                                    uint8_t* __restrict__ y, Q8Args a) {
+  const int parts = a.D / 8;
+  const long n = (long)blockIdx.x * 256 + threadIdx.x;
+  const long row = n / parts;
+  const int part = (int)(n % parts);
+  if (row >= (long)a.B * a.H * a.s_pad) return;   // whole rows, so whole 4-lane groups
+  const int s = (int)(row % a.s_pad);
+  const long bh = row / a.s_pad;
+  const int h = (int)(bh % a.H);
+  const long b = bh / a.H;
+  u32x4 v = u32x4{0u, 0u, 0u, 0u};
+  if (s < a.S) v = *(const u32x4*)(x + ((b * a.S + s) * a.H + h) * a.D + part * 8);
+  unsigned am = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) am = max(am, max(v[i] & 0x7fffu, (v[i] >> 16) & 0x7fffu));
+  am = max(am, (unsigned)__shfl_xor((int)am, 1));
+  am = max(am, (unsigned)__shfl_xor((int)am, 2));
+  const int e = (int)(am >> 7);
+  const int k = e == 0 ? -127 : max(e - 135, -127);
+  unsigned w[2] = {0u, 0u};
+#pragma unroll
+  for (int j = 0; j < 8; ++j) w[j >> 2] |= e4m3_code((v[j >> 1] >> (16 * (j & 1))) & 0xffffu, k) << (8 * (j & 3));
+  *(uint2*)(y + row * a.D + part * 8) = make_uint2(w[0], w[1]);
+  if ((part & 3) == 0) y[a.soff + row * (a.D / 32) + (part >> 2)] = (uint8_t)(k + 127);
+}
+
 // ------------------------------------------------------ fused attention
 struct AttnArgs {
   int B, Sq, Sk, Hq, Hkv;
@@ -434,6 +487,9 @@ struct AttnArgs {
   float* row_m;
   float* row_l;
   int nblk;           // ceil(Sk / 32)
+  // MXFP8 Q^ / K^ (low-bit Q K^T): padded rows per head, scale offsets
+  int sq_pad, sk_pad;
+  size_t q8_soff, k8_soff;
 };
 
 // LDS layout.  A K tile is stored in the order the bf16 MFMA reads its A
@@ -447,10 +503,12 @@ struct AttnArgs {
 // K and V~ have three buffers each: step j reads K of tile j+1 and V~ of
 // tile j while K of tile j+3 and V~ of tile j+2 stream in, so a load has
 // two steps to land.
+// With MXFP8 Q and K (Q8) a K tile holds E4M3 codes in the order the FP8
+// MFMA reads its A operand (see KLoad8), then 256 bytes of E8M0 scales.
 constexpr int kStages = 3;    // ring depth of the four-wave kernel
-template <int D, int KS = kStages, int VS = kStages>
+template <int D, int KS = kStages, int VS = kStages, bool Q8 = false>
 struct Smem {
-  static constexpr int kK = kBc * D * 2;                 // one K tile
+  static constexpr int kK = Q8 ? kBc * D + 256 : kBc * D * 2;   // one K tile
   static constexpr int kVc = 2 * D * 16;                 // V~ codes of two blocks
   static constexpr int kVs = 256;                        // V~ scales (2 D bytes, padded)
   static constexpr int kV = kVc + kVs;                   // one V~ tile
@@ -524,6 +582,47 @@ struct VLoad {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, vbuf + Smem<D>::kVc, 4, (lane % (2 * D / 4)) * 4,
                                                tile * 2 * D, 0, 0);
     }
+  }
+};
+
+// MXFP8 K tiles (low-bit Q K^T).  The FP8 MFMA (32x32x64, E4M3) reads its A
+// operand as 32 bytes per lane: lane l holds row l % 32 and, of a 64-column
+// chunk, columns 16 (l / 32) + [0, 16) in bytes 0-15 and 32 + 16 (l / 32) +
+// [0, 16) in bytes 16-31.  The LDS tile stores 1 KB blocks (window w, chunk
+// c, half h) at ((w * D/64 + c) * 2 + h) KB, slot `lane` of the block holding
+// the lane's 16 bytes of half h, so an operand is two contiguous wave reads;
+// each block is one direct-to-LDS load.  The 64 keys' E8M0 scales follow
+// (D/32 bytes per key, as in global memory).  Global K^ is [batch][kv head]
+// [padded key][D] codes and [..][D/32] scales, so a tile is contiguous.
+template <int D, int NW>
+struct KLoad8 {
+  static constexpr int NC = D / 64;                      // 64-column chunks
+  static constexpr int NBLK = 4 * NC;                    // 1 KB code blocks per tile
+  static_assert(NBLK <= NW, "one code block per wave");
+  static constexpr int SW = NW - 2;                      // the wave that loads the scales
+  const void* codes;
+  const void* scales;
+  unsigned cbytes, sbytes;
+  int voff;                                              // lane's byte offset in its block's rows
+  __device__ void init(const uint8_t* kc, const uint8_t* ks, int sk_pad, int wave, int lane) {
+    codes = kc;
+    scales = ks;
+    cbytes = (unsigned)sk_pad * D;
+    sbytes = (unsigned)sk_pad * (D / 32);
+    const int blk = wave < NBLK ? wave : 0;
+    const int h = blk & 1, c = (blk >> 1) % NC, w = blk / (2 * NC);
+    voff = (32 * w + (lane & 31)) * D + 64 * c + 32 * h + 16 * (lane >> 5);
+  }
+  __device__ static int issued(int wave) { return (wave < NBLK ? 1 : 0) + (wave == SW ? 1 : 0); }
+  __device__ void issue(uint8_t* kbuf, int tile, int wave, int lane) const {
+    if (wave < NBLK)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(codes, cbytes), kbuf + wave * 1024, 16,
+                                               voff, tile * kBc * D, 0, 0);
+    // 64 keys x D/32 bytes as dwords; for D = 64 the upper lanes read the
+    // next tile's scales (or zeros past the end) into the unused half
+    if (wave == SW)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(scales, sbytes), kbuf + kBc * D, 4,
+                                               lane * 4, tile * kBc * (D / 32), 0, 0);
   }
 };
 
@@ -921,8 +1020,8 @@ constexpr int kPPThreads = 64 * kPPWaves;
 constexpr int kPP = EFQ_PREFETCH;          // tiles streamed ahead (>= 2)
 constexpr int kPPK = kPP + 1;              // K ring depth
 constexpr int kPPV = kPP + 2;              // V~ ring depth
-template <int D>
-using SmemPP = Smem<D, kPPK, kPPV>;
+template <int D, bool Q8 = false>
+using SmemPP = Smem<D, kPPK, kPPV, Q8>;
 
 // P~1 on the 16x16x128 FP4 MFMA.  Its B operand is the P~^T operand of the
 // P~V product as it sits in the lanes (lane l: query l % 32, key block
@@ -1002,10 +1101,115 @@ __device__ __forceinline__ PgenOut mma_phase(const uint8_t* kbuf, const bf16x8* 
   return po;
 }
 
-template <int D, int KIND, bool DUMP>
+// Q operand of the Q K^T MFMAs, held in registers for the whole kernel:
+// bf16 (B operand of the 32x32x16 MFMA, 8 columns per k-step), or MXFP8
+// (B operand of the FP8 32x32x64 MFMA per 64-column chunk, and in byte c of
+// `sc` the E8M0 scale the lane supplies for chunk c).
+template <int D, bool Q8>
+struct QOps {
+  bf16x8 r[D / 16];
+};
+template <int D>
+struct QOps<D, true> {
+  i32x8 a[D / 64];
+  int sc;
+};
+
+// The E8M0 scale of 32 columns of a row that lane (row, half) supplies to
+// the FP8 MFMA of chunk c is that of columns 64 c + 32 half + [0, 32): from
+// the row's D/32 scale bytes `raw`, byte c of the result is byte 2 c + half.
+template <int D>
+__device__ __forceinline__ int lane_scales(unsigned raw, int half) {
+  const unsigned x = raw >> (8 * half);
+  if constexpr (D == 128) return (int)((x & 0xffu) | ((x >> 8) & 0xff00u));
+  else return (int)(x & 0xffu);
+}
+
+// A operand (K rows of window I % 2, chunk I / 2) of MXFP8 region I from an
+// LDS K tile, and the lane's K scales of window w.
+template <int D>
+__device__ __forceinline__ i32x8 k8_operand(const uint8_t* kb, int lane, int region) {
+  constexpr int NC = D / 64;
+  const uint8_t* p = kb + (((region & 1) * NC + (region >> 1)) * 2) * 1024 + lane * 16;
+  const u32x4 lo = *(const u32x4*)p;
+  const u32x4 hi = *(const u32x4*)(p + 1024);
+  return i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
+               (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+}
+
+template <int D>
+__device__ __forceinline__ int k8_scales(const uint8_t* kb, int lane, int w) {
+  const int key = 32 * w + (lane & 31);
+  const uint8_t* sp = kb + kBc * D;
+  unsigned raw;
+  if constexpr (D == 128) raw = *(const unsigned*)(sp + key * 4);
+  else raw = *(const unsigned short*)(sp + key * 2);
+  return lane_scales<D>(raw, lane >> 5);
+}
+
+// Matrix phase with MXFP8 Q and K: S = K Q^T of one 64-key tile on the FP8
+// MFMA with E8M0 block scales, one MFMA per region (window I % 2, chunk
+// I / 2, alternating windows so consecutive MFMAs are independent), the LDS
+// operand reads PD regions ahead; the code slices of the previous tile are
+// spread over the regions as in the bf16 path.
+template <int D, int KIND, bool QK, int I>
+__device__ __forceinline__ void mc_regions8(const uint8_t* kb, int lane, i32x8* ka,
+                                            const QOps<D, true>& qo, int ks0, int ks1,
+                                            f32x16& sn0, f32x16& sn1, const f32x16& sc0,
+                                            const f32x16& sc1, const PgenArgs& pa,
+                                            PgenState& st) {
+  constexpr int R = D / 32;
+  constexpr int PD = R < 2 ? R : 2;
+  if constexpr (I < R) {
+    if constexpr (QK) {
+      constexpr int C = I >> 1;
+      if constexpr ((I & 1) == 0)
+        sn0 = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ka[I], qo.a[C], sn0, 0, 0, C, ks0, C, qo.sc);
+      else
+        sn1 = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ka[I], qo.a[C], sn1, 0, 0, C, ks1, C, qo.sc);
+      if constexpr (I + PD < R) ka[I + PD] = k8_operand<D>(kb, lane, I + PD);
+    }
+    constexpr int P0 = 16 * I / R, P1 = 16 * (I + 1) / R;
+    pg_pairs<KIND, 2 * P0, 2 * P1>(sc0, sc1, pa, st);
+    __builtin_amdgcn_sched_barrier(0);
+    mc_regions8<D, KIND, QK, I + 1>(kb, lane, ka, qo, ks0, ks1, sn0, sn1, sc0, sc1, pa, st);
+  }
+}
+
+template <int D, int KIND, bool QK, bool CODES>
+__device__ __forceinline__ PgenOut mma_phase8(const uint8_t* kbuf, const QOps<D, true>& qo,
+                                              int lane, f32x16& sn0, f32x16& sn1,
+                                              const f32x16& sc0, const f32x16& sc1,
+                                              const PgenArgs& pa, PgenState& st) {
+  constexpr int R = D / 32;
+  constexpr int PD = R < 2 ? R : 2;
+  i32x8 ka[R];
+  int ks0 = 0, ks1 = 0;
+  if constexpr (QK) {
+#pragma unroll
+    for (int i = 0; i < PD; ++i) ka[i] = k8_operand<D>(kbuf, lane, i);
+    ks0 = k8_scales<D>(kbuf, lane, 0);
+    ks1 = k8_scales<D>(kbuf, lane, 1);
+    sn0 = f32x16{};
+    sn1 = f32x16{};
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  PgenOut po{};
+  if constexpr (CODES) {
+    mc_regions8<D, KIND, QK, 0>(kbuf, lane, ka, qo, ks0, ks1, sn0, sn1, sc0, sc1, pa, st);
+    if constexpr (KIND == EFQ_PGEN_NOOP) asm volatile("" ::"v"(sc0), "v"(sc1));
+    po = pg_finish<KIND>(st);
+  } else {
+    f32x16 z{};
+    mc_regions8<D, EFQ_PGEN_NOOP, QK, 0>(kbuf, lane, ka, qo, ks0, ks1, sn0, sn1, z, z, pa, st);
+  }
+  return po;
+}
+
+template <int D, int KIND, bool DUMP, bool Q8 = false>
 struct PPWave {
   static constexpr int NS = D / 32;
-  bf16x8 qreg[D / 16];
+  QOps<D, Q8> qo;
   f32x16 oacc[NS];
   f32x4 lacc;             // element 0: the lane's row sum l
   i32x8 sel;              // A operand of the P~1 MFMA
@@ -1021,8 +1225,10 @@ struct PPWave {
   __device__ __forceinline__ void mphase(int j, const uint8_t* kbuf0, const VOps<D>& vop,
                                          const AttnArgs& a, int b, int hq, f32x16& sn0,
                                          f32x16& sn1, const f32x16& sc0, const f32x16& sc1) {
-    const uint8_t* kb = kbuf0 + ((QK ? j : 0) % kPPK) * SmemPP<D>::kK;
-    PgenOut po = mma_phase<D, KIND, QK, CODES>(kb, qreg, lane, sn0, sn1, sc0, sc1, pa, st);
+    const uint8_t* kb = kbuf0 + ((QK ? j : 0) % kPPK) * SmemPP<D, Q8>::kK;
+    PgenOut po;
+    if constexpr (Q8) po = mma_phase8<D, KIND, QK, CODES>(kb, qo, lane, sn0, sn1, sc0, sc1, pa, st);
+    else po = mma_phase<D, KIND, QK, CODES>(kb, qo.r, lane, sn0, sn1, sc0, sc1, pa, st);
     if constexpr (CODES) {
       if constexpr (DUMP) {
         const int blk = 2 * (j - 1) + half;
@@ -1044,7 +1250,7 @@ struct PPWave {
   // and rescale the history when a row maximum moved.
   __device__ __forceinline__ void vphase(int j, const uint8_t* vbuf0, f32x16& s0, f32x16& s1,
                                          VOps<D>& vop) {
-    read_v<D>(vbuf0 + (j % kPPV) * SmemPP<D>::kV, lane, vop);
+    read_v<D>(vbuf0 + (j % kPPV) * SmemPP<D, Q8>::kV, lane, vop);
     const int lim = vis_end - j * kBc;
     if (__builtin_amdgcn_ballot_w64(lim < kBc) != 0ull) mask_tile(s0, s1, lim, half);
     float pm0, pm1;
@@ -1071,8 +1277,8 @@ struct PPWave {
 // V~(j-2) in a ring of P+2) were last read, and the reads consumed, by
 // phase 2j-1.  Every wave passes 2 ntiles + 2 barriers.  Scores alternate
 // between two register sets.
-template <int G, int D, int KIND, bool DUMP, typename Stream>
-__device__ __forceinline__ void pp_schedule(PPWave<D, KIND, DUMP>& w, int T, int ntiles,
+template <int G, int D, int KIND, bool DUMP, bool Q8, typename Stream>
+__device__ __forceinline__ void pp_schedule(PPWave<D, KIND, DUMP, Q8>& w, int T, int ntiles,
                                             const uint8_t* kbuf0, const uint8_t* vbuf0,
                                             const AttnArgs& a, int b, int hq,
                                             const int (&fifo0)[kPP - 1], Stream stream) {
@@ -1120,14 +1326,17 @@ __device__ __forceinline__ void pp_schedule(PPWave<D, KIND, DUMP>& w, int T, int
   while (t < 2 * ntiles + 2) { begin(); end(); }
 }
 
-template <int D, int KIND, bool CAUSAL, bool DUMP>
+// Q8: q and k are the MXFP8 buffers Q^ and K^ (E4M3 codes, then E8M0 scales
+// at a.q8_soff / a.k8_soff, [batch][head][padded seq] rows), else bf16 BSHD.
+template <int D, int KIND, bool CAUSAL, bool DUMP, bool Q8>
 __global__ __attribute__((amdgpu_flat_work_group_size(kPPThreads, kPPThreads),
                           amdgpu_waves_per_eu(2, 2))) void
-attn_pp_kernel(const unsigned short* __restrict__ q, const unsigned short* __restrict__ k,
+attn_pp_kernel(const void* __restrict__ q, const void* __restrict__ k,
                const uint8_t* __restrict__ vhat, float* __restrict__ out, AttnArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
   constexpr int KK = D / 16;
   constexpr int NS = D / 32;
+  using Sm = SmemPP<D, Q8>;
 
   int b, hq, qt;
   map_work(a, b, hq, qt);
@@ -1135,16 +1344,33 @@ attn_pp_kernel(const unsigned short* __restrict__ q, const unsigned short* __res
   // wave index as a uniform (scalar) value: the group branch below is uniform
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int group = wave >> 2;
-  PPWave<D, KIND, DUMP> w;
+  PPWave<D, KIND, DUMP, Q8> w;
   w.lane = threadIdx.x & 63;
   w.half = w.lane >> 5;
   const int q_wave0 = qt * kPPBr + wave * kWaveQ;
   w.my_q = q_wave0 + (w.lane & 31);
   const int q_load = w.my_q < a.Sq ? w.my_q : a.Sq - 1;
-  {
-    const unsigned short* qp = q + (((long)b * a.Sq + q_load) * a.Hq + hq) * D + w.half * 8;
+  if constexpr (Q8) {
+    const uint8_t* qh = (const uint8_t*)q;
+    const long row = ((long)b * a.Hq + hq) * a.sq_pad + q_load;
+    const uint8_t* qp = qh + row * D + 16 * w.half;
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) w.qreg[kk] = *(const bf16x8*)(qp + kk * 16);
+    for (int c = 0; c < D / 64; ++c) {
+      const u32x4 lo = *(const u32x4*)(qp + 64 * c);
+      const u32x4 hi = *(const u32x4*)(qp + 64 * c + 32);
+      w.qo.a[c] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
+                        (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+    }
+    const uint8_t* sp = qh + a.q8_soff + row * (D / 32);
+    unsigned raw;
+    if constexpr (D == 128) raw = *(const unsigned*)sp;
+    else raw = *(const unsigned short*)sp;
+    w.qo.sc = lane_scales<D>(raw, w.half);
+  } else {
+    const unsigned short* qp =
+        (const unsigned short*)q + (((long)b * a.Sq + q_load) * a.Hq + hq) * D + w.half * 8;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) w.qo.r[kk] = *(const bf16x8*)(qp + kk * 16);
   }
   // tiles of the workgroup and of this wave (1 <= wtiles <= ntiles)
   const int kv_end = CAUSAL ? min(a.Sk, qt * kPPBr + kPPBr) : a.Sk;
@@ -1153,13 +1379,22 @@ attn_pp_kernel(const unsigned short* __restrict__ q, const unsigned short* __res
   const int wtiles = (wave_end + kBc - 1) / kBc;
   w.vis_end = CAUSAL ? min(a.Sk, w.my_q + 1) : a.Sk;
 
-  KLoad<D, kPPWaves> kload;
-  kload.init(k + (long)b * a.Sk * a.Hkv * D, a.Sk, a.Hkv, g, wave, w.lane);
+  std::conditional_t<Q8, KLoad8<D, kPPWaves>, KLoad<D, kPPWaves>> kload;
+  int k_issued;
+  if constexpr (Q8) {
+    const uint8_t* kh = (const uint8_t*)k;
+    const long hrow = ((long)b * a.Hkv + g) * a.sk_pad;
+    kload.init(kh + hrow * D, kh + a.k8_soff + hrow * (D / 32), a.sk_pad, wave, w.lane);
+    k_issued = KLoad8<D, kPPWaves>::issued(wave);
+  } else {
+    kload.init((const unsigned short*)k + (long)b * a.Sk * a.Hkv * D, a.Sk, a.Hkv, g, wave, w.lane);
+    k_issued = KLoad<D, kPPWaves>::kIssued;
+  }
   VLoad<D, kPPWaves> vload;
   vload.init(vhat + ((long)b * a.Hkv + g) * a.nb * D * 16,
              vhat + a.scale_off + ((long)b * a.Hkv + g) * a.nb * D, a.nb);
-  uint8_t* const kbuf0 = smem + SmemPP<D>::kKOff;
-  uint8_t* const vbuf0 = smem + SmemPP<D>::kVOff;
+  uint8_t* const kbuf0 = smem + Sm::kKOff;
+  uint8_t* const vbuf0 = smem + Sm::kVOff;
   const int v_issued = VLoad<D, kPPWaves>::issued(wave);
 
   w.pa.scale = a.scale;
@@ -1178,9 +1413,10 @@ attn_pp_kernel(const unsigned short* __restrict__ q, const unsigned short* __res
   // exists; returns the number of loads issued.
   auto load_tile = [&](int x) {
     if (x >= ntiles) return 0;
-    kload.issue(kbuf0 + (x % kPPK) * SmemPP<D>::kK, x, wave);
-    vload.issue(vbuf0 + (x % kPPV) * SmemPP<D>::kV, x, wave, w.lane);
-    return KLoad<D, kPPWaves>::kIssued + v_issued;
+    if constexpr (Q8) kload.issue(kbuf0 + (x % kPPK) * Sm::kK, x, wave, w.lane);
+    else kload.issue(kbuf0 + (x % kPPK) * Sm::kK, x, wave);
+    vload.issue(vbuf0 + (x % kPPV) * Sm::kV, x, wave, w.lane);
+    return k_issued + v_issued;
   };
   // prologue: tiles 0 .. P; tiles 0 and 1 resident, 2 .. P in flight (the
   // loads of the last P-1 even phases before phase 2)
@@ -1468,7 +1704,7 @@ int launch_vquant(const void* v, const efq_shape* s, void* vhat, hipStream_t st)
   return EFQ_OK;
 }
 
-template <int D, int KIND, bool CAUSAL, bool DUMP>
+template <int D, int KIND, bool CAUSAL, bool DUMP, bool Q8>
 hipError_t launch_attn_t(const void* q, const void* k, const void* vhat, float* out,
                          const AttnArgs& a, hipStream_t st, unsigned grid) {
 #if EFQ_PINGPONG
@@ -1476,16 +1712,17 @@ hipError_t launch_attn_t(const void* q, const void* k, const void* vhat, float* 
   // call is idempotent, so a race between threads is harmless)
   static bool lds_ok = false;
   if (!lds_ok) {
-    hipError_t e = hipFuncSetAttribute((const void*)attn_pp_kernel<D, KIND, CAUSAL, DUMP>,
+    hipError_t e = hipFuncSetAttribute((const void*)attn_pp_kernel<D, KIND, CAUSAL, DUMP, Q8>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       SmemPP<D>::kTotal);
+                                       SmemPP<D, Q8>::kTotal);
     if (e != hipSuccess) return e;
     lds_ok = true;
   }
-  hipLaunchKernelGGL((attn_pp_kernel<D, KIND, CAUSAL, DUMP>), dim3(grid), dim3(kPPThreads),
-                     SmemPP<D>::kTotal, st, (const unsigned short*)q, (const unsigned short*)k,
-                     (const uint8_t*)vhat, out, a);
+  constexpr int lds = SmemPP<D, Q8>::kTotal;
+  hipLaunchKernelGGL((attn_pp_kernel<D, KIND, CAUSAL, DUMP, Q8>), dim3(grid), dim3(kPPThreads),
+                     lds, st, q, k, (const uint8_t*)vhat, out, a);
 #else
+  if constexpr (Q8) return hipErrorNotSupported;
   hipLaunchKernelGGL((attn_fwd_kernel<D, KIND, CAUSAL, DUMP>), dim3(grid), dim3(kThreads),
                      Smem<D>::kTotal, st, (const unsigned short*)q, (const unsigned short*)k,
                      (const uint8_t*)vhat, out, a);
@@ -1493,13 +1730,13 @@ hipError_t launch_attn_t(const void* q, const void* k, const void* vhat, float* 
   return hipGetLastError();
 }
 
-template <int D, bool DUMP>
+template <int D, bool DUMP, bool Q8>
 hipError_t launch_attn_d(int kind, bool causal, const void* q, const void* k, const void* vhat,
                          float* out, const AttnArgs& a, hipStream_t st, unsigned grid) {
-#define EFQ_CASE(KIND)                                                                   \
-  case KIND:                                                                             \
-    return causal ? launch_attn_t<D, KIND, true, DUMP>(q, k, vhat, out, a, st, grid)     \
-                  : launch_attn_t<D, KIND, false, DUMP>(q, k, vhat, out, a, st, grid);
+#define EFQ_CASE(KIND)                                                                    \
+  case KIND:                                                                              \
+    return causal ? launch_attn_t<D, KIND, true, DUMP, Q8>(q, k, vhat, out, a, st, grid)  \
+                  : launch_attn_t<D, KIND, false, DUMP, Q8>(q, k, vhat, out, a, st, grid);
   switch (kind) {
     EFQ_CASE(EFQ_PGEN_EFQ)
     EFQ_CASE(EFQ_PGEN_EXPQ)
@@ -1510,16 +1747,43 @@ hipError_t launch_attn_d(int kind, bool causal, const void* q, const void* k, co
   }
   if constexpr (!DUMP) {
     if (kind == EFQ_PGEN_NOOP)
-      return causal ? launch_attn_t<D, EFQ_PGEN_NOOP, true, false>(q, k, vhat, out, a, st, grid)
-                    : launch_attn_t<D, EFQ_PGEN_NOOP, false, false>(q, k, vhat, out, a, st, grid);
+      return causal ? launch_attn_t<D, EFQ_PGEN_NOOP, true, false, Q8>(q, k, vhat, out, a, st, grid)
+                    : launch_attn_t<D, EFQ_PGEN_NOOP, false, false, Q8>(q, k, vhat, out, a, st, grid);
   }
 #undef EFQ_CASE
   return hipErrorInvalidValue;
 }
 
+size_t round256(size_t n) { return (n + 255) & ~(size_t)255; }
+long pad64(int n) { return 64L * ((n + 63) / 64); }
+
+// MXFP8 Q^ / K^ buffers: rows = batch * heads * padded seq
+size_t q8_scale_offset(long rows, int D) { return round256((size_t)rows * D); }
+size_t q8_bytes(long rows, int D) { return q8_scale_offset(rows, D) + round256((size_t)rows * (D / 32)); }
+long qhat_rows(const efq_shape* s) { return (long)s->batch * s->heads_q * pad64(s->seq_q); }
+long khat_rows(const efq_shape* s) { return (long)s->batch * s->heads_kv * pad64(s->seq_k); }
+
+int launch_q8(const void* x, int B, int S, int H, int D, void* y, hipStream_t st) {
+  Q8Args a;
+  a.B = B;
+  a.S = S;
+  a.H = H;
+  a.D = D;
+  a.s_pad = (int)pad64(S);
+  const long rows = (long)B * H * a.s_pad;
+  a.soff = q8_scale_offset(rows, D);
+  const long threads = rows * (D / 8);
+  hipLaunchKernelGGL(mxfp8_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st,
+                     (const unsigned short*)x, (uint8_t*)y, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(EFQ_EHIP, "mxfp8 launch: %s", hipGetErrorString(e));
+  return EFQ_OK;
+}
+
+// q8: q and k are the MXFP8 buffers Q^ and K^ of this shape.
 int launch_attn(const void* q, const void* k, const void* vhat, float scale, int causal, int kind,
                 efq_params p, float* out, const efq_shape* s, hipStream_t st, uint8_t* p_codes,
-                uint8_t* p_e8m0, float* row_m, float* row_l) {
+                uint8_t* p_e8m0, float* row_m, float* row_l, bool q8 = false) {
   AttnArgs a;
   a.B = s->batch;
   a.Sq = s->seq_q;
@@ -1539,14 +1803,28 @@ int launch_attn(const void* q, const void* k, const void* vhat, float scale, int
   a.nblk = (s->seq_k + 31) / 32;
   const long total = (long)a.B * a.Hq * a.nqt;
   a.xcd_remap = (total % 8 == 0) ? 1 : 0;
+  a.sq_pad = (int)pad64(s->seq_q);
+  a.sk_pad = (int)pad64(s->seq_k);
+  a.q8_soff = q8_scale_offset(qhat_rows(s), s->head_dim);
+  a.k8_soff = q8_scale_offset(khat_rows(s), s->head_dim);
   const bool dump = p_codes != nullptr;
+  const unsigned g = (unsigned)total;
   hipError_t e;
-  if (s->head_dim == 64)
-    e = dump ? launch_attn_d<64, true>(kind, causal, q, k, vhat, out, a, st, (unsigned)total)
-             : launch_attn_d<64, false>(kind, causal, q, k, vhat, out, a, st, (unsigned)total);
-  else
-    e = dump ? launch_attn_d<128, true>(kind, causal, q, k, vhat, out, a, st, (unsigned)total)
-             : launch_attn_d<128, false>(kind, causal, q, k, vhat, out, a, st, (unsigned)total);
+  if (s->head_dim == 64) {
+    if (q8)
+      e = dump ? launch_attn_d<64, true, true>(kind, causal, q, k, vhat, out, a, st, g)
+               : launch_attn_d<64, false, true>(kind, causal, q, k, vhat, out, a, st, g);
+    else
+      e = dump ? launch_attn_d<64, true, false>(kind, causal, q, k, vhat, out, a, st, g)
+               : launch_attn_d<64, false, false>(kind, causal, q, k, vhat, out, a, st, g);
+  } else {
+    if (q8)
+      e = dump ? launch_attn_d<128, true, true>(kind, causal, q, k, vhat, out, a, st, g)
+               : launch_attn_d<128, false, true>(kind, causal, q, k, vhat, out, a, st, g);
+    else
+      e = dump ? launch_attn_d<128, true, false>(kind, causal, q, k, vhat, out, a, st, g)
+               : launch_attn_d<128, false, false>(kind, causal, q, k, vhat, out, a, st, g);
+  }
   if (e != hipSuccess) return fail(EFQ_EHIP, "attention launch: %s", hipGetErrorString(e));
   return EFQ_OK;
 }
@@ -1662,6 +1940,139 @@ int efq_attn_fwd_expq(const void* q, const void* k, const void* v, float scale, 
                       float* out, const efq_shape* s, efq_stream_t stream) {
   return efq_attn_fwd_ex(q, k, v, scale, causal, EFQ_PGEN_EXPQ, efq_params{EFQ_TAU_MEAN, EFQ_H_MEAN},
                          out, s, nullptr, 0, stream);
+}
+
+// ------------------------------------------------ low-bit Q K^T (MXFP8)
+size_t efq_qhat_bytes(const efq_shape* s) {
+  if (validate_shape(s, 0) != EFQ_OK) return 0;
+  return q8_bytes(qhat_rows(s), s->head_dim);
+}
+size_t efq_qhat_scale_offset(const efq_shape* s) {
+  if (validate_shape(s, 0) != EFQ_OK) return 0;
+  return q8_scale_offset(qhat_rows(s), s->head_dim);
+}
+size_t efq_khat_bytes(const efq_shape* s) {
+  if (validate_shape(s, 0) != EFQ_OK) return 0;
+  return q8_bytes(khat_rows(s), s->head_dim);
+}
+size_t efq_khat_scale_offset(const efq_shape* s) {
+  if (validate_shape(s, 0) != EFQ_OK) return 0;
+  return q8_scale_offset(khat_rows(s), s->head_dim);
+}
+
+int efq_quant_qk_mxfp8(const void* q, const void* k, const efq_shape* s, void* qhat,
+                       size_t qhat_nbytes, void* khat, size_t khat_nbytes, efq_stream_t stream) {
+  int rc = validate_shape(s, 0);
+  if (rc) return rc;
+  if (!q || !k || !qhat || !khat) return fail(EFQ_EINVAL, "null pointer");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(qhat) || !aligned16(khat))
+    return fail(EFQ_EINVAL, "pointers must be 16-byte aligned");
+  const size_t nq = q8_bytes(qhat_rows(s), s->head_dim), nk = q8_bytes(khat_rows(s), s->head_dim);
+  if (qhat_nbytes < nq) return fail(EFQ_EWORKSPACE, "qhat needs %zu bytes, got %zu", nq, qhat_nbytes);
+  if (khat_nbytes < nk) return fail(EFQ_EWORKSPACE, "khat needs %zu bytes, got %zu", nk, khat_nbytes);
+  if ((rc = check_device())) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  rc = launch_q8(q, s->batch, s->seq_q, s->heads_q, s->head_dim, qhat, st);
+  if (rc == EFQ_OK) rc = launch_q8(k, s->batch, s->seq_k, s->heads_kv, s->head_dim, khat, st);
+  return rc;
+}
+
+static int check_qk8_args(const void* qhat, size_t qhat_nbytes, const void* khat,
+                          size_t khat_nbytes, const void* vhat, size_t vhat_nbytes, float scale,
+                          int causal, int kind, bool allow_noop, efq_params p, const float* out,
+                          const efq_shape* s) {
+  int rc = validate_shape(s, causal);
+  if (rc) return rc;
+  if (!qhat || !khat || !vhat || !out) return fail(EFQ_EINVAL, "null pointer");
+  if (!aligned16(qhat) || !aligned16(khat) || !aligned16(vhat) || !aligned16(out))
+    return fail(EFQ_EINVAL, "pointers must be 16-byte aligned");
+  if ((rc = check_kind(kind, allow_noop)) || (rc = check_params(p)) || (rc = check_scale(scale)))
+    return rc;
+  const size_t nq = q8_bytes(qhat_rows(s), s->head_dim), nk = q8_bytes(khat_rows(s), s->head_dim);
+  if (qhat_nbytes < nq) return fail(EFQ_EWORKSPACE, "qhat needs %zu bytes, got %zu", nq, qhat_nbytes);
+  if (khat_nbytes < nk) return fail(EFQ_EWORKSPACE, "khat needs %zu bytes, got %zu", nk, khat_nbytes);
+  if (vhat_nbytes < vhat_bytes(s))
+    return fail(EFQ_EWORKSPACE, "vhat needs %zu bytes, got %zu", vhat_bytes(s), vhat_nbytes);
+  return EFQ_OK;
+}
+
+int efq_attn_fwd_qk8(const void* qhat, size_t qhat_nbytes, const void* khat, size_t khat_nbytes,
+                     const void* vhat, size_t vhat_nbytes, float scale, int causal, int kind,
+                     efq_params p, float* out, const efq_shape* s, efq_stream_t stream) {
+  int rc = check_qk8_args(qhat, qhat_nbytes, khat, khat_nbytes, vhat, vhat_nbytes, scale, causal,
+                          kind, true, p, out, s);
+  if (rc) return rc;
+  if ((rc = check_device())) return rc;
+  return launch_attn(qhat, khat, vhat, scale, causal, kind, p, out, s, (hipStream_t)stream,
+                     nullptr, nullptr, nullptr, nullptr, true);
+}
+
+int efq_attn_fwd_qk8_dump(const void* qhat, size_t qhat_nbytes, const void* khat,
+                          size_t khat_nbytes, const void* vhat, size_t vhat_nbytes, float scale,
+                          int causal, int kind, efq_params p, float* out, const efq_shape* s,
+                          uint8_t* p_codes, uint8_t* p_e8m0, float* row_m, float* row_l,
+                          efq_stream_t stream) {
+  int rc = check_qk8_args(qhat, qhat_nbytes, khat, khat_nbytes, vhat, vhat_nbytes, scale, causal,
+                          kind, false, p, out, s);
+  if (rc) return rc;
+  if (!p_codes || !p_e8m0 || !row_m || !row_l) return fail(EFQ_EINVAL, "null pointer");
+  if (!aligned16(p_codes)) return fail(EFQ_EINVAL, "pointers must be 16-byte aligned");
+  if ((long)s->batch * s->heads_q * s->seq_q > (1L << 24))
+    return fail(EFQ_EUNSUPPORTED, "dump is for small shapes (batch*heads_q*seq_q <= 2^24)");
+  if ((rc = check_device())) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  const size_t rows = (size_t)s->batch * s->heads_q * s->seq_q;
+  const size_t nblk = (size_t)(s->seq_k + 31) / 32;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(1024), dim3(256), 0, st, p_codes, rows * nblk * 16);
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(1024), dim3(256), 0, st, p_e8m0, rows * nblk);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(EFQ_EHIP, "fill launch: %s", hipGetErrorString(e));
+  return launch_attn(qhat, khat, vhat, scale, causal, kind, p, out, s, st, p_codes, p_e8m0, row_m,
+                     row_l, true);
+}
+
+size_t efq_attn_lowbit_workspace_bytes(const efq_shape* s) {
+  if (validate_shape(s, 0) != EFQ_OK) return 0;
+  return round256(q8_bytes(qhat_rows(s), s->head_dim)) +
+         round256(q8_bytes(khat_rows(s), s->head_dim)) + vhat_bytes(s);
+}
+
+int efq_attn_fwd_lowbit_ex(const void* q, const void* k, const void* v, float scale, int causal,
+                           int kind, efq_params p, float* out, const efq_shape* s, void* ws,
+                           size_t ws_bytes, efq_stream_t stream) {
+  int rc = validate_shape(s, causal);
+  if (rc) return rc;
+  if (!q || !k || !v || !out) return fail(EFQ_EINVAL, "null pointer");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
+    return fail(EFQ_EINVAL, "pointers must be 16-byte aligned");
+  if ((rc = check_kind(kind, true)) || (rc = check_params(p)) || (rc = check_scale(scale))) return rc;
+  const size_t nq = round256(q8_bytes(qhat_rows(s), s->head_dim));
+  const size_t nk = round256(q8_bytes(khat_rows(s), s->head_dim));
+  const size_t need = nq + nk + vhat_bytes(s);
+  if (ws_bytes != 0 && (!ws || ws_bytes < need))
+    return fail(EFQ_EWORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  if (ws && ((uintptr_t)ws & 255u) != 0) return fail(EFQ_EINVAL, "workspace must be 256-byte aligned");
+  if ((rc = check_device())) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  void* buf = ws;
+  if (ws_bytes == 0) {
+    hipError_t e = hipMallocAsync(&buf, need, st);
+    if (e != hipSuccess) return fail(EFQ_EHIP, "hipMallocAsync(%zu): %s", need, hipGetErrorString(e));
+  }
+  uint8_t* qh = (uint8_t*)buf;
+  uint8_t* kh = qh + nq;
+  uint8_t* vh = kh + nk;
+  rc = launch_q8(q, s->batch, s->seq_q, s->heads_q, s->head_dim, qh, st);
+  if (rc == EFQ_OK) rc = launch_q8(k, s->batch, s->seq_k, s->heads_kv, s->head_dim, kh, st);
+  if (rc == EFQ_OK) rc = launch_vquant(v, s, vh, st);
+  if (rc == EFQ_OK)
+    rc = launch_attn(qh, kh, vh, scale, causal, kind, p, out, s, st, nullptr, nullptr, nullptr,
+                     nullptr, true);
+  if (ws_bytes == 0) {
+    hipError_t e = hipFreeAsync(buf, st);
+    if (rc == EFQ_OK && e != hipSuccess) rc = fail(EFQ_EHIP, "hipFreeAsync: %s", hipGetErrorString(e));
+  }
+  return rc;
 }
 
 // Workspace of efq_calibrate: V~, one output, the reduction partials and

@@ -135,3 +135,52 @@ def test_valid_call_without_gpu_reports_hip_error(L):
         pytest.skip("a GPU is present: the GPU tests cover valid calls")
     assert call_vhat(L, shape()) == L.EFQ_EHIP
     assert "hip" in L.lib().efq_strerror(L.EFQ_EHIP).decode().lower()
+
+
+def test_lowbit_sizes(L):
+    """Q^ / K^ layout sizes: rows padded to 64 per (batch, head), codes then
+    scales, each part a multiple of 256 bytes."""
+    lib = L.lib()
+    s = shape(batch=2, seq_q=75, seq_k=130, heads_q=6, heads_kv=3, head_dim=128)
+    r256 = lambda n: (n + 255) // 256 * 256
+    rq, rk = 2 * 6 * 128, 2 * 3 * 192
+    assert lib.efq_qhat_scale_offset(ctypes.byref(s)) == r256(rq * 128)
+    assert lib.efq_qhat_bytes(ctypes.byref(s)) == r256(rq * 128) + r256(rq * 4)
+    assert lib.efq_khat_scale_offset(ctypes.byref(s)) == r256(rk * 128)
+    assert lib.efq_khat_bytes(ctypes.byref(s)) == r256(rk * 128) + r256(rk * 4)
+    assert lib.efq_attn_lowbit_workspace_bytes(ctypes.byref(s)) == (
+        lib.efq_qhat_bytes(ctypes.byref(s)) + lib.efq_khat_bytes(ctypes.byref(s)) + L.vhat_bytes(s))
+    assert lib.efq_qhat_bytes(ctypes.byref(shape(head_dim=96))) == 0
+
+
+def test_lowbit_arguments(L):
+    lib = L.lib()
+    s = shape()
+    nq, nk, nv = (lib.efq_qhat_bytes(ctypes.byref(s)), lib.efq_khat_bytes(ctypes.byref(s)),
+                  L.vhat_bytes(s))
+    P = L.Params(-3.06, 2.3)
+
+    def qk8(qh=FAKE, a=nq, kh=FAKE, b=nk, c=nv, kind=0, causal=0, sh=s, scale=0.125):
+        return lib.efq_attn_fwd_qk8(qh, a, kh, b, FAKE, c, scale, causal, kind, P, FAKE,
+                                    ctypes.byref(sh), None)
+    assert qk8(qh=None) == L.EFQ_EINVAL
+    assert qk8(kh=ctypes.c_void_p(4104)) == L.EFQ_EINVAL
+    assert qk8(a=nq - 1) == L.EFQ_EWORKSPACE
+    assert qk8(b=nk - 1) == L.EFQ_EWORKSPACE
+    assert qk8(c=nv - 1) == L.EFQ_EWORKSPACE
+    assert qk8(kind=9) == L.EFQ_EINVAL
+    assert qk8(scale=-1.0) == L.EFQ_EINVAL
+    assert qk8(sh=shape(seq_q=100, seq_k=200), causal=1) == L.EFQ_EUNSUPPORTED
+    assert lib.efq_attn_fwd_qk8_dump(FAKE, nq, FAKE, nk, FAKE, nv, 0.125, 0, 3, P, FAKE,
+                                     ctypes.byref(s), FAKE, FAKE, FAKE, FAKE, None) == L.EFQ_EINVAL
+    assert lib.efq_attn_fwd_qk8_dump(FAKE, nq, FAKE, nk, FAKE, nv, 0.125, 0, 0, P, FAKE,
+                                     ctypes.byref(s), None, FAKE, FAKE, FAKE, None) == L.EFQ_EINVAL
+    assert lib.efq_quant_qk_mxfp8(FAKE, FAKE, ctypes.byref(s), FAKE, nq, FAKE, nk - 1,
+                                  None) == L.EFQ_EWORKSPACE
+    assert lib.efq_quant_qk_mxfp8(FAKE, None, ctypes.byref(s), FAKE, nq, FAKE, nk,
+                                  None) == L.EFQ_EINVAL
+    ex = lambda ws, n: lib.efq_attn_fwd_lowbit_ex(FAKE, FAKE, FAKE, 0.125, 0, 0, P, FAKE,
+                                                  ctypes.byref(s), ws, n, None)
+    need = lib.efq_attn_lowbit_workspace_bytes(ctypes.byref(s))
+    assert ex(FAKE, need - 1) == L.EFQ_EWORKSPACE
+    assert ex(ctypes.c_void_p(4096 + 16), need) == L.EFQ_EINVAL   # not 256-byte aligned
