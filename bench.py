@@ -13,6 +13,9 @@ Besides the headline TFLOP/s it reports
     exp-then-quantize, in microseconds per 128x128 score tile on one CU,
     and the exposed stage cost inside the fused kernel (policy minus a
     no-op probability stage);
+  * lowbit: the low-bit variant (MXFP8 Q and K, Q K^T on the FP8 matrix
+    core) on the same workload, its fused kernel against the FP8 / MXFP4
+    peaks, per probability stage;
   * cpu_baseline: the CPU oracle on a bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -29,6 +32,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16 = 2500.0     # TFLOP/s, MI355X dense bf16 MFMA
 PEAK_FP4 = 10100.0     # TFLOP/s, MI355X dense MXFP4 MFMA
+PEAK_FP8 = 5000.0      # TFLOP/s, MI355X dense FP8 MFMA
 N_CU = 256
 COPY_BYTES = 1 << 30   # plain copy used to scale the HBM counters
 
@@ -239,6 +243,9 @@ def main():
         }
         result["policies"] = extra
 
+    if not args.no_extra:
+        result["lowbit"] = lowbit_run(w, binding, q, k, v, vhat, out, stream, args.steps)
+
     if not args.no_extra and args.target_workload:
         result["target"] = target_run(args, binding, inputs, dev, stream)
 
@@ -287,6 +294,64 @@ def sweep(args, binding, inputs, dev):
         torch.cuda.empty_cache()
 
 
+def _time_calls(fn, n, stream):
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(n):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / n
+
+
+def lowbit_run(w, binding, q, k, v, vhat, out, stream, steps):
+    """Low-bit Q K^T on the same inputs: the MXFP8 pre-pass of Q and K, the
+    MXFP4 pre-pass of V, then the fused kernel with the FP8 Q K^T.  Fused
+    kernel time per probability stage (and the exposed stage cost against
+    the no-op stage), the pre-pass time, and the whole step."""
+    import torch
+    sh = binding.shape_of(q, k)
+    qh, kh = binding.quant_qk(q, k, stream=stream)
+    binding.quant_v(v, seq_q=w.seq, heads_q=w.heads_q, out=vhat, stream=stream)
+    peak = 1.0 / (0.5 / PEAK_FP8 + 0.5 / PEAK_FP4)
+    n = max(5, steps // 2)
+    res = {"qk": "mxfp8 (e4m3, e8m0 per 32)", "peak": round(peak, 1), "unit": "TFLOP/s"}
+    for kind in ("efq", "expq", "expq6", "noop"):
+        prm = binding.PARAMS_MEAN
+
+        def call(kind=kind, prm=prm):
+            binding.attn_fwd_qk8(qh, kh, vhat, sh, w.scale, w.causal, kind, prm, out=out,
+                                 stream=stream)
+        for _ in range(2):
+            call()
+        torch.cuda.synchronize()
+        ms = _time_calls(call, n, stream)
+        tf = w.flops() / (ms * 1e-3) / 1e12
+        res[kind] = {"attn_ms": round(ms, 4), "tflops": round(tf, 2), "frac": round(tf / peak, 4)}
+    ex = {kd: res[kd]["attn_ms"] - res["noop"]["attn_ms"] for kd in ("efq", "expq", "expq6")}
+    res["exposed_ms"] = {kd: round(x, 4) for kd, x in ex.items()}
+    res["exposed_speedup_vs_expq"] = round(1 - ex["efq"] / ex["expq"], 4) if ex["expq"] > 0 else None
+
+    def prepass():
+        binding.quant_qk(q, k, stream=stream)
+    res["qk_prepass_ms"] = round(_time_calls(prepass, n, stream), 4)
+    ws = torch.empty(binding.lowbit_workspace_bytes(sh) + 256, dtype=torch.uint8, device=q.device)
+    off = (-ws.data_ptr()) % 256
+    wsv = ws[off: off + binding.lowbit_workspace_bytes(sh)]
+
+    def whole():
+        binding.attn_fwd_lowbit(q, k, v, w.scale, w.causal, "efq", out=out, workspace=wsv,
+                                stream=stream)
+    whole()
+    torch.cuda.synchronize()
+    ms = _time_calls(whole, n, stream)
+    res["step_ms"] = round(ms, 4)
+    res["step_tflops"] = round(w.flops() / (ms * 1e-3) / 1e12, 2)
+    del qh, kh, ws
+    return res
+
+
 def target_run(args, binding, inputs, dev, stream):
     """The fused kernel on a second workload (the 32K-token Qwen3-8B heads),
     timed like the headline one; attention kernel only."""
@@ -312,7 +377,22 @@ def target_run(args, binding, inputs, dev, stream):
         ms = e0.elapsed_time(e1) / n
         tf = w.flops() / (ms * 1e-3) / 1e12
         res[kind] = {"attn_ms": round(ms, 4), "tflops": round(tf, 2), "frac": round(tf / peak, 4)}
-    del q, k, v, vh, out
+    # the low-bit variant (MXFP8 Q K^T) of the EFQ kernel
+    sh = binding.shape_of(q, k)
+    qh, kh = binding.quant_qk(q, k, stream=stream)
+    peak8 = 1.0 / (0.5 / PEAK_FP8 + 0.5 / PEAK_FP4)
+
+    def call():
+        binding.attn_fwd_qk8(qh, kh, vh, sh, w.scale, w.causal, "efq", binding.PARAMS_MEAN,
+                             out=out, stream=stream)
+    for _ in range(2):
+        call()
+    torch.cuda.synchronize()
+    ms = _time_calls(call, max(3, args.steps // 4), stream)
+    tf = w.flops() / (ms * 1e-3) / 1e12
+    res["lowbit_efq"] = {"attn_ms": round(ms, 4), "tflops": round(tf, 2),
+                         "frac": round(tf / peak8, 4), "peak": round(peak8, 1)}
+    del q, k, v, vh, out, qh, kh
     torch.cuda.empty_cache()
     return res
 
