@@ -1008,18 +1008,27 @@ __global__ __launch_bounds__(kThreads, EFQ_WAVES_PER_SIMD) void attn_fwd_kernel(
 // the other runs the probability stage:
 //   phase 2j:    group 0 runs M(j),  group 1 runs V(j-1)
 //   phase 2j+1:  group 0 runs V(j),  group 1 runs M(j)
-// K(j) is read in phases 2j and 2j+1, V~(j) in phases 2j+2 and 2j+3.  Both
-// stream through three-stage rings, issued at an even phase four phases
-// before their first use and waited for at the end of the next phase.
+// K(j) is read in phases 2j-1 .. 2j+1 (the first operands of a matrix phase
+// are read in the VALU phase before it), V~(j) in phases 2j+1 and 2j+2.
+// Both stream through LDS rings (schedule and ring depths at pp_schedule).
 constexpr int kPPWaves = 8;
 constexpr int kPPBr = kWaveQ * kPPWaves;   // queries per workgroup
 constexpr int kPPThreads = 64 * kPPWaves;
+#ifndef EFQ_KPRE
+#define EFQ_KPRE 1                         // read K operands one phase early
+#endif
 #ifndef EFQ_PREFETCH
-#define EFQ_PREFETCH 2
+#define EFQ_PREFETCH (2 + EFQ_KPRE)
 #endif
 constexpr int kPP = EFQ_PREFETCH;          // tiles streamed ahead (>= 2)
 constexpr int kPPK = kPP + 1;              // K ring depth
 constexpr int kPPV = kPP + 2;              // V~ ring depth
+#ifndef EFQ_KPRE_BF16
+#define EFQ_KPRE_BF16 0                    // also on the bf16 Q K^T path
+#endif
+constexpr bool kKPre = EFQ_KPRE != 0;
+constexpr int kKeep = kPP - 1 - (kKPre ? 1 : 0);   // batches left in flight at odd phases
+static_assert(kKeep >= 0, "prefetch distance too short for the K pre-read");
 template <int D, bool Q8 = false>
 using SmemPP = Smem<D, kPPK, kPPV, Q8>;
 
@@ -1069,19 +1078,26 @@ __device__ __forceinline__ void mc_regions(const uint8_t* p0, const uint8_t* p1,
   }
 }
 
-template <int D, int KIND, bool QK, bool CODES>
-__device__ __forceinline__ PgenOut mma_phase(const uint8_t* kbuf, const bf16x8* qreg, int lane,
-                                             f32x16& sn0, f32x16& sn1, const f32x16& sc0,
-                                             const f32x16& sc1, const PgenArgs& pa,
-                                             PgenState& st) {
+template <int D, bool Q8>
+struct KPre;
+
+template <int D, int KIND, bool QK, bool CODES, bool PRE>
+__device__ __forceinline__ PgenOut mma_phase(const uint8_t* kbuf, const bf16x8* qreg,
+                                             const KPre<D, false>& kp, int lane, f32x16& sn0,
+                                             f32x16& sn1, const f32x16& sc0, const f32x16& sc1,
+                                             const PgenArgs& pa, PgenState& st) {
   constexpr int KK = D / 16;
   constexpr int PD = KK < 3 ? KK : 3;
   const uint8_t* p0 = kbuf + lane * 16;
   const uint8_t* p1 = p0 + KK * 1024;
   bf16x8 a0[KK], a1[KK];
   if constexpr (QK) {
+    if constexpr (PRE) {
+      a0[0] = kp.a0;
+      a1[0] = kp.a1;
+    }
 #pragma unroll
-    for (int kk = 0; kk < PD; ++kk) {
+    for (int kk = PRE ? 1 : 0; kk < PD; ++kk) {
       a0[kk] = *(const bf16x8*)(p0 + kk * 1024);
       a1[kk] = *(const bf16x8*)(p1 + kk * 1024);
     }
@@ -1176,20 +1192,52 @@ __device__ __forceinline__ void mc_regions8(const uint8_t* kb, int lane, i32x8* 
   }
 }
 
-template <int D, int KIND, bool QK, bool CODES>
+// K operands of the first Q K^T MFMAs of a tile, read from LDS in the VALU
+// phase before its matrix phase, so the matrix phase starts without waiting
+// for LDS: bf16, the first k-step of both windows; MXFP8, the first two
+// regions and both windows' scales.
+template <int D, bool Q8>
+struct KPre {
+  bf16x8 a0, a1;
+  __device__ __forceinline__ void read(const uint8_t* kb, int lane) {
+    a0 = *(const bf16x8*)(kb + lane * 16);
+    a1 = *(const bf16x8*)(kb + lane * 16 + (D / 16) * 1024);
+  }
+};
+template <int D>
+struct KPre<D, true> {
+  i32x8 k0, k1;   // regions 0 and 1
+  int ks0, ks1;
+  __device__ __forceinline__ void read(const uint8_t* kb, int lane) {
+    k0 = k8_operand<D>(kb, lane, 0);
+    k1 = k8_operand<D>(kb, lane, 1);
+    ks0 = k8_scales<D>(kb, lane, 0);
+    ks1 = k8_scales<D>(kb, lane, 1);
+  }
+};
+
+template <int D, int KIND, bool QK, bool CODES, bool PRE>
 __device__ __forceinline__ PgenOut mma_phase8(const uint8_t* kbuf, const QOps<D, true>& qo,
-                                              int lane, f32x16& sn0, f32x16& sn1,
-                                              const f32x16& sc0, const f32x16& sc1,
+                                              const KPre<D, true>& kp, int lane, f32x16& sn0,
+                                              f32x16& sn1, const f32x16& sc0, const f32x16& sc1,
                                               const PgenArgs& pa, PgenState& st) {
   constexpr int R = D / 32;
   constexpr int PD = R < 2 ? R : 2;
+  static_assert(PD == 2, "the pre-read covers the first two regions");
   i32x8 ka[R];
   int ks0 = 0, ks1 = 0;
   if constexpr (QK) {
+    if constexpr (PRE) {
+      ka[0] = kp.k0;
+      ka[1] = kp.k1;
+      ks0 = kp.ks0;
+      ks1 = kp.ks1;
+    } else {
 #pragma unroll
-    for (int i = 0; i < PD; ++i) ka[i] = k8_operand<D>(kbuf, lane, i);
-    ks0 = k8_scales<D>(kbuf, lane, 0);
-    ks1 = k8_scales<D>(kbuf, lane, 1);
+      for (int i = 0; i < PD; ++i) ka[i] = k8_operand<D>(kbuf, lane, i);
+      ks0 = k8_scales<D>(kbuf, lane, 0);
+      ks1 = k8_scales<D>(kbuf, lane, 1);
+    }
     sn0 = f32x16{};
     sn1 = f32x16{};
   }
@@ -1217,18 +1265,24 @@ struct PPWave {
   PgenArgs pa;
   PgenState st;           // block parameters of the tile between V(j) and M(j+1)
   int lane, half, my_q, vis_end;
+  // the pre-read needs registers the bf16 exp-then-quantize variants lack
+  static constexpr bool kPreOn = kKPre && (Q8 || EFQ_KPRE_BF16);
 
   // Matrix phase M(j): with QK the scores of tile j into sn, and with CODES
   // the codes of tile j-1 (scores sc) in the shadow of those MFMAs, then its
-  // P~V and P~1 MFMAs.
-  template <bool QK, bool CODES>
+  // P~V and P~1 MFMAs.  PRE: the first K operands are in kp.
+  template <bool QK, bool CODES, bool PRE>
   __device__ __forceinline__ void mphase(int j, const uint8_t* kbuf0, const VOps<D>& vop,
-                                         const AttnArgs& a, int b, int hq, f32x16& sn0,
-                                         f32x16& sn1, const f32x16& sc0, const f32x16& sc1) {
+                                         const KPre<D, Q8>& kp, const AttnArgs& a, int b, int hq,
+                                         f32x16& sn0, f32x16& sn1, const f32x16& sc0,
+                                         const f32x16& sc1) {
     const uint8_t* kb = kbuf0 + ((QK ? j : 0) % kPPK) * SmemPP<D, Q8>::kK;
+    constexpr bool P = PRE && kPreOn;
     PgenOut po;
-    if constexpr (Q8) po = mma_phase8<D, KIND, QK, CODES>(kb, qo, lane, sn0, sn1, sc0, sc1, pa, st);
-    else po = mma_phase<D, KIND, QK, CODES>(kb, qo.r, lane, sn0, sn1, sc0, sc1, pa, st);
+    if constexpr (Q8)
+      po = mma_phase8<D, KIND, QK, CODES, P>(kb, qo, kp, lane, sn0, sn1, sc0, sc1, pa, st);
+    else
+      po = mma_phase<D, KIND, QK, CODES, P>(kb, qo.r, kp, lane, sn0, sn1, sc0, sc1, pa, st);
     if constexpr (CODES) {
       if constexpr (DUMP) {
         const int blk = 2 * (j - 1) + half;
@@ -1244,12 +1298,16 @@ struct PPWave {
     }
   }
 
-  // VALU phase V(j): read the V~(j) operands for the next matrix phase, mask
-  // the scores of tile j (diagonal and ragged tiles only), take the block
-  // and row maxima and the block parameters (row maximum, alpha, k_b, bias),
-  // and rescale the history when a row maximum moved.
-  __device__ __forceinline__ void vphase(int j, const uint8_t* vbuf0, f32x16& s0, f32x16& s1,
-                                         VOps<D>& vop) {
+  // VALU phase V(j): read the V~(j) operands for the next matrix phase (and
+  // the first K operands of tile j+1: after the last tile the read lands in
+  // an unused slot and its values are never used), mask the scores of tile
+  // j (diagonal and ragged tiles only), take the block and row maxima and
+  // the block parameters (row maximum, alpha, k_b, bias), and rescale the
+  // history when a row maximum moved.  The reads are unconditional so the
+  // operands stay in registers.
+  __device__ __forceinline__ void vphase(int j, const uint8_t* vbuf0, const uint8_t* kbuf0,
+                                         f32x16& s0, f32x16& s1, VOps<D>& vop, KPre<D, Q8>& kp) {
+    if constexpr (kPreOn) kp.read(kbuf0 + ((j + 1) % kPPK) * SmemPP<D, Q8>::kK, lane);
     read_v<D>(vbuf0 + (j % kPPV) * SmemPP<D, Q8>::kV, lane, vop);
     const int lim = vis_end - j * kBc;
     if (__builtin_amdgcn_ballot_w64(lim < kBc) != 0ull) mask_tile(s0, s1, lim, half);
@@ -1267,16 +1325,18 @@ struct PPWave {
 // The per-wave schedule of the ping-pong kernel.  A wave with T tiles runs
 // M(0) V(0) M(1) V(1) ... M(T-1) V(T-1) F, where M(j) also codes tile j-1
 // and applies its P~V (j >= 1) and F codes and applies the last tile; group
-// G runs op o in phase o + G, so K(j) is read in phases 2j, 2j+1 and V~(j)
-// in phases 2j+1, 2j+2.  Phase t ends with a barrier; even phases t = 2j
-// >= 2 start by streaming tile j+P (K and V~), odd phases end by waiting
-// until only the loads of the last P-1 even phases are outstanding (loads
-// complete in order).  A load issued in phase 2j has therefore landed by
-// the end of phase 2(j+P)-1, in time for K(j+P) in phase 2(j+P) and V~(j+P)
-// in phase 2(j+P)+1; the slots it overwrites (K(j-1) in a ring of P+1,
-// V~(j-2) in a ring of P+2) were last read, and the reads consumed, by
-// phase 2j-1.  Every wave passes 2 ntiles + 2 barriers.  Scores alternate
-// between two register sets.
+// G runs op o in phase o + G.  K(j) is read in phases 2j-1 .. 2j+1 (V(j-1)
+// reads the first operands of M(j) with the K pre-read, else from 2j on)
+// and V~(j) in phases 2j+1, 2j+2.  Phase t ends with a barrier; even phases
+// t = 2j >= 2 start by streaming tile j+P (K and V~), odd phases end by
+// waiting until only the loads of the last E even phases are outstanding
+// (loads complete in order), E = P-2 with the pre-read, else P-1.  A load
+// issued in phase 2j has therefore landed by the end of phase 2(j+P-E)-1:
+// with the pre-read (P = 3, E = 1) that is 2(j+P)-3, in time for the
+// pre-read of K(j+P) in phase 2(j+P)-1.  The slots it overwrites (K(j-1) in
+// a ring of P+1, V~(j-2) in a ring of P+2) were last read, and the reads
+// consumed, by phase 2j-1.  Every wave passes 2 ntiles + 2 barriers.
+// Scores alternate between two register sets.
 template <int G, int D, int KIND, bool DUMP, bool Q8, typename Stream>
 __device__ __forceinline__ void pp_schedule(PPWave<D, KIND, DUMP, Q8>& w, int T, int ntiles,
                                             const uint8_t* kbuf0, const uint8_t* vbuf0,
@@ -1284,6 +1344,7 @@ __device__ __forceinline__ void pp_schedule(PPWave<D, KIND, DUMP, Q8>& w, int T,
                                             const int (&fifo0)[kPP - 1], Stream stream) {
   f32x16 sa0, sa1, sb0, sb1;
   VOps<D> vop;
+  KPre<D, Q8> kp;      // first K operands of the next matrix phase
   int fifo[kPP - 1];   // loads issued by the last P-1 even phases, oldest first
 #pragma unroll
   for (int i = 0; i < kPP - 1; ++i) fifo[i] = fifo0[i];
@@ -1299,29 +1360,30 @@ __device__ __forceinline__ void pp_schedule(PPWave<D, KIND, DUMP, Q8>& w, int T,
     if (t & 1) {
       int n = 0;
 #pragma unroll
-      for (int i = 0; i < kPP - 1; ++i) n += fifo[i];
+      for (int i = kPP - 1 - kKeep; i < kPP - 1; ++i) n += fifo[i];
       wait_vmem_le(n);
     }
     wg_barrier();
     ++t;
   };
   if (G == 1) { begin(); end(); }
-  // M(0), V(0)
-  begin(); w.template mphase<true, false>(0, kbuf0, vop, a, b, hq, sa0, sa1, sb0, sb1); end();
-  begin(); w.vphase(0, vbuf0, sa0, sa1, vop); end();
+  // M(0), V(0); every later M(j) with Q K^T follows a V(j-1) that pre-read
+  // its first K operands (j < T)
+  begin(); w.template mphase<true, false, false>(0, kbuf0, vop, kp, a, b, hq, sa0, sa1, sb0, sb1); end();
+  begin(); w.vphase(0, vbuf0, kbuf0, sa0, sa1, vop, kp); end();
   int j = 1;
   for (; j + 1 < T; j += 2) {
-    begin(); w.template mphase<true, true>(j, kbuf0, vop, a, b, hq, sb0, sb1, sa0, sa1); end();
-    begin(); w.vphase(j, vbuf0, sb0, sb1, vop); end();
-    begin(); w.template mphase<true, true>(j + 1, kbuf0, vop, a, b, hq, sa0, sa1, sb0, sb1); end();
-    begin(); w.vphase(j + 1, vbuf0, sa0, sa1, vop); end();
+    begin(); w.template mphase<true, true, true>(j, kbuf0, vop, kp, a, b, hq, sb0, sb1, sa0, sa1); end();
+    begin(); w.vphase(j, vbuf0, kbuf0, sb0, sb1, vop, kp); end();
+    begin(); w.template mphase<true, true, true>(j + 1, kbuf0, vop, kp, a, b, hq, sa0, sa1, sb0, sb1); end();
+    begin(); w.vphase(j + 1, vbuf0, kbuf0, sa0, sa1, vop, kp); end();
   }
   if (j < T) {   // one more tile: its scores go to set b, the last coded from b
-    begin(); w.template mphase<true, true>(j, kbuf0, vop, a, b, hq, sb0, sb1, sa0, sa1); end();
-    begin(); w.vphase(j, vbuf0, sb0, sb1, vop); end();
-    begin(); w.template mphase<false, true>(T, kbuf0, vop, a, b, hq, sa0, sa1, sb0, sb1); end();
+    begin(); w.template mphase<true, true, true>(j, kbuf0, vop, kp, a, b, hq, sb0, sb1, sa0, sa1); end();
+    begin(); w.vphase(j, vbuf0, kbuf0, sb0, sb1, vop, kp); end();
+    begin(); w.template mphase<false, true, false>(T, kbuf0, vop, kp, a, b, hq, sa0, sa1, sb0, sb1); end();
   } else {       // the last tile's scores are in set a
-    begin(); w.template mphase<false, true>(T, kbuf0, vop, a, b, hq, sb0, sb1, sa0, sa1); end();
+    begin(); w.template mphase<false, true, false>(T, kbuf0, vop, kp, a, b, hq, sb0, sb1, sa0, sa1); end();
   }
   while (t < 2 * ntiles + 2) { begin(); end(); }
 }
