@@ -289,8 +289,26 @@ def sweep(args, binding, inputs, dev):
         ex = {kd: res[kd]["attn_ms"] - noop for kd in ("efq", "expq", "expq6", "lut")}
         res["exposed_ms"] = {kd: round(x, 4) for kd, x in ex.items()}
         res["exposed_speedup_vs_expq"] = round(1 - ex["efq"] / ex["expq"], 4) if ex["expq"] > 0 else None
+        # low-bit Q K^T (MXFP8 Q and K)
+        sh = binding.shape_of(q, k)
+        qh, kh = binding.quant_qk(q, k, stream=stream)
+        peak8 = 1.0 / (0.5 / PEAK_FP8 + 0.5 / PEAK_FP4)
+        lb = {}
+        for kind in ("efq", "expq", "noop"):
+            def call(kind=kind):
+                binding.attn_fwd_qk8(qh, kh, vh, sh, w.scale, True, kind, binding.PARAMS_MEAN,
+                                     out=out, stream=stream)
+            for _ in range(3):
+                call()
+            torch.cuda.synchronize()
+            ms = _time_calls(call, n, stream)
+            tf = w.flops() / (ms * 1e-3) / 1e12
+            lb[kind] = {"attn_ms": round(ms, 4), "tflops": round(tf, 1), "frac": round(tf / peak8, 4)}
+        exl = {kd: lb[kd]["attn_ms"] - lb["noop"]["attn_ms"] for kd in ("efq", "expq")}
+        lb["exposed_speedup_vs_expq"] = round(1 - exl["efq"] / exl["expq"], 4) if exl["expq"] > 0 else None
+        res["lowbit"] = lb
         print(json.dumps(res), flush=True)
-        del q, k, v, vh, out
+        del q, k, v, vh, out, qh, kh
         torch.cuda.empty_cache()
 
 

@@ -1,6 +1,6 @@
 """Text summaries of rocprofv3 output for the profiles/ folder.
 
-traffic FETCH_DIR WRITE_DIR WORKLOAD
+traffic FETCH_DIR WRITE_DIR WORKLOAD [OUT_FILE]
     HBM traffic per launch of the attention kernel from two counter runs of
     `bench.py --pmc-run` (one with FETCH_SIZE, one with WRITE_SIZE).  Both
     counters are scaled by what they read for the plain device copy of
@@ -13,6 +13,9 @@ stats TRACE_DIR OUT_FILE COMMAND...
     Kernel-time summary of a `rocprofv3 --kernel-trace --stats` run: the
     per-kernel statistics, and per launch configuration (grid size) the
     calls and average duration of the attention kernels.
+
+sweep JSONL OUT_FILE COMMAND...
+    Table of a `bench.py --sweep` run (one JSON line per sequence length).
 """
 from __future__ import annotations
 
@@ -82,13 +85,41 @@ def stats(trace_dir: str, out: str, command: str):
     print(open(out).read())
 
 
+def sweep(jsonl: str, out: str, command: str):
+    import json
+    rows = [json.loads(l) for l in open(jsonl) if l.strip().startswith("{")]
+    with open(out, "w") as fh:
+        fh.write("# fused attention kernel time per sequence length, Qwen3-8B heads "
+                 "(32 q / 8 kv, D 128, causal), HIP events on the launch stream\n")
+        fh.write(f"# command (from the repository root):\n#   {command}\n")
+        fh.write("# exposed = t(policy) - t(no-op probability stage); speedup = 1 - exposed(EFQ) / "
+                 "exposed(exp-then-quantize)\n")
+        fh.write("# seq | efq ms | expq ms | expq6 ms | lut ms | noop ms | efq TFLOP/s | frac | "
+                 "exposed speedup | low-bit efq ms | low-bit expq ms | low-bit noop ms | "
+                 "low-bit frac | low-bit exposed speedup\n")
+        for r in rows:
+            lb = r.get("lowbit", {})
+            g = lambda d, k: d.get(k, {}).get("attn_ms", float("nan"))
+            fh.write(f"{r['seq']} | {g(r, 'efq'):.3f} | {g(r, 'expq'):.3f} | {g(r, 'expq6'):.3f} | "
+                     f"{g(r, 'lut'):.3f} | {g(r, 'noop'):.3f} | {r['efq']['tflops']} | "
+                     f"{r['efq']['frac']} | {r['exposed_speedup_vs_expq']} | {g(lb, 'efq'):.3f} | "
+                     f"{g(lb, 'expq'):.3f} | {g(lb, 'noop'):.3f} | "
+                     f"{lb.get('efq', {}).get('frac')} | {lb.get('exposed_speedup_vs_expq')}\n")
+    print(open(out).read())
+
+
 def main():
     if sys.argv[1] == "stats":
         stats(sys.argv[2], sys.argv[3], " ".join(sys.argv[4:]))
         return
+    if sys.argv[1] == "sweep":
+        sweep(sys.argv[2], sys.argv[3], " ".join(sys.argv[4:]))
+        return
     import bench
     from paper_2609_09721_amd import inputs
     fetch_dir, write_dir, wl = sys.argv[2], sys.argv[3], sys.argv[4]
+    out = sys.argv[5] if len(sys.argv) > 5 else os.path.join(ROOT, "profiles",
+                                                             f"attn_fwd_{wl}_traffic.txt")
     is_attn = lambda n: "attn_pp_kernel" in n or "attn_fwd_kernel" in n
     is_copy = lambda n: "copyBuffer" in n
     f = per_dispatch(fetch_dir, "FETCH_SIZE")
@@ -105,7 +136,6 @@ def main():
             + w.batch * w.seq * w.heads_kv * w.head_dim * 2            # K bf16
             + w.batch * w.heads_kv * 2 * ((w.seq + 63) // 64) * w.head_dim * 17  # V~
             + w.batch * w.seq * w.heads_q * w.head_dim * 4)            # O fp32
-    out = os.path.join(ROOT, "profiles", f"attn_fwd_{wl}_traffic.txt")
     with open(out, "w") as fh:
         fh.write(f"# HBM traffic of one attention launch, {wl} (EFQ), from rocprofv3 counters\n")
         fh.write("# commands (from the repository root, TMPDIR=/tmp):\n")
