@@ -19,7 +19,9 @@
  *     Eq. (d8-index) for the code (EFQ), or the 16-level index j16 folded by
  *     the table C16 of Sec. II-D (EFQ-Softmax-LUT).
  *   - Exp-then-quantize baseline (pgen_block_expq): Eq. (post-softmax-path):
- *     FP32 probabilities exp(x), then the OCP MXFP4 quantiser.
+ *     FP32 probabilities exp(x), then the OCP MXFP4 quantiser, or (ORC_EXPQ6)
+ *     the "scale6" exponent ceil(log2(amax / 6)) of the paper's comparison
+ *     rows (Sec. IV).
  *   - Low-bit Q K^T (orc_quant_mxfp8, orc_attn with qk8 set): the paper
  *     frames low-bit attention as running Q K^T (and P V) on FP8/FP4 matrix
  *     engines (Sec. I).  Q and K are then MXFP8 under the OCP microscaling
@@ -28,7 +30,9 @@
  *     rounded to nearest (ties to even), saturating at 448.
  *   - The online recurrence (orc_attn): Algorithm 2 for every key/value tile
  *     in ascending order: Eqs. (rowmax-update), (alpha), (numerator-basic),
- *     (denominator-basic) and the final division of Sec. III-A.
+ *     (denominator-basic) and the final division of Sec. III-A.  Algorithm 3
+ *     (the offline (tau, h) search of Sec. III-C) is a loop over this call,
+ *     in oracle/__init__.py.
  *
  * Floating point.  The accumulators (A, l) and the exact-softmax reference
  * are fp64.  The decisions that produce integers (scale exponent k_b, code
