@@ -86,6 +86,15 @@ __device__ __forceinline__ void swap32f(float& a, float& b) {
   b = __uint_as_float(ub);
 }
 
+// Maximum of two values that came through an integer lane swap: an IEEE
+// maximum would first quiet each operand (two more instructions); scores
+// are never NaN, so the plain instruction is exact.
+__device__ __forceinline__ float fmax_swapped(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
 // Maximum of 16 values as a depth-3 tree of three-input maxima (v_max3):
 // eight instructions with short dependency chains instead of a serial chain.
 __device__ __forceinline__ float max3f(float a, float b, float c) {
@@ -190,10 +199,10 @@ __device__ __forceinline__ void pg_params(float pm0, float pm1, float& m, const 
     constexpr bool LOG2 = is_expq<KIND>();
     const float unit = LOG2 ? pa.l2s : pa.scale;
     swap32f(pm0, pm1);                          // lower: (own, partner) block 0; upper: block 1
-    const float bmine = __builtin_fmaxf(pm0, pm1);   // raw maximum of the lane's own block
+    const float bmine = fmax_swapped(pm0, pm1);  // raw maximum of the lane's own block
     float t0 = bmine, t1 = bmine;
     swap32f(t0, t1);                            // (block 0 max, block 1 max) in every lane
-    const float mt = __builtin_fmaxf(t0, t1) * unit;   // rowmax S^j (monotone in the raw max)
+    const float mt = fmax_swapped(t0, t1) * unit;   // rowmax S^j (monotone in the raw max)
     const float mnew = __builtin_fmaxf(m, mt);
     // alpha = exp(m^{j-1} - m^j), Eq. (alpha); exactly 1 when the max is unchanged
     const float d = LOG2 ? (m - mnew) : (m - mnew) * kInvLn2;
