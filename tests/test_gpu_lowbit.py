@@ -128,6 +128,19 @@ def test_qk8_expq_exact_scores(B, orc, kind):
     assert np.max(np.abs(og - oo)) <= TOL
 
 
+def _mxfp8_abs_torch(x):
+    """|MXFP8 value| of x [..., D] (bf16, any device) by torch's own float8
+    cast (round to nearest even; the scale makes |x| / 2^k < 512 and values
+    above 448 are clamped first, as the MX rule saturates), fp32."""
+    xf = x.float().reshape(*x.shape[:-1], -1, 32)
+    amax = xf.abs().amax(dim=-1, keepdim=True)
+    _, e = torch.frexp(amax)
+    k = torch.where(amax > 0, (e - 9).clamp(-127, 127), torch.full_like(e, -127)).double()
+    y = (xf.double() / torch.exp2(k)).clamp(-448, 448).float()
+    v = y.to(torch.float8_e4m3fn).double() * torch.exp2(k)
+    return v.abs().float().reshape(x.shape)
+
+
 def _absdot_bound(orc, q, k, w):
     """Per row (b, hq, i) in oracle order: D 2^-23 max_t sum_d |q^_d k^_t,d|,
     a bound on the difference between fp32 accumulation in any order and
@@ -204,27 +217,31 @@ def test_lowbit_same_operand_v_constant(B):
         assert float((out + 2.0).abs().max()) <= 1e-6 * 16
 
 
-def test_lowbit_fullsize_sampled_rows(B, orc):
-    """Qwen3-8B at 32K, causal: the benchmark's low-bit path at full size on
+@pytest.mark.parametrize("wl", ["qwen3_8b_16k", "qwen3_8b_32k", "qwen3_8b_128k", "qwen3_vl_32k",
+                                "wan22_75600"])
+def test_lowbit_fullsize_sampled_rows(B, orc, wl):
+    """Every benchmark workload at full size through the low-bit path, on
     sampled rows; rows over the tolerance must be explained by a decision
     within fp32 accumulation error of its threshold, and be rare."""
-    w = inputs.WORKLOADS["qwen3_8b_32k"]
+    w = inputs.WORKLOADS[wl]
     print(f"[lowbit] fullsize {w.name}", flush=True)
     dev = torch.device("cuda:0")
     q, k, v = inputs.make_qkv(w, device=dev)
     out = B.attn_fwd_lowbit(q, k, v, w.scale, w.causal, "efq")
     torch.cuda.synchronize()
     assert bool(torch.isfinite(out).all())
-    rows = inputs.sample_rows(w, 128, seed=12).numpy()
+    rows = inputs.sample_rows(w, 96, seed=12).numpy()
     got = out[rows[:, 0], rows[:, 2], rows[:, 1]].cpu().numpy()
     del out
     group = w.heads_q // w.heads_kv
     absdot = np.zeros(len(rows))
+    kcache = {}
     for n, (b, hq, i) in enumerate(rows.tolist()):
-        ka = k[b, :, hq // group].float().abs()
-        absdot[n] = float((ka @ q[b, i, hq].float().abs()).max())
-    # E4M3 rounding changes a magnitude by at most a factor 1 + 2^-4
-    bound = w.head_dim * 2.0 ** -23 * absdot * (1 + 2 ** -4) ** 2
+        key = (b, hq // group)
+        if key not in kcache:
+            kcache = {key: _mxfp8_abs_torch(k[b, :, hq // group])}
+        absdot[n] = float((kcache[key] @ _mxfp8_abs_torch(q[b, i, hq][None])[0]).max())
+    bound = w.head_dim * 2.0 ** -23 * absdot
     ref, margin = orc.attn(orc.bf16_bits(q), orc.bf16_bits(k), orc.bf16_bits(v), w.scale,
                            w.causal, orc.EFQ, bc=64, rows=rows, margins=True, qk8=True)
     err = np.abs(got - ref).max(axis=1)
