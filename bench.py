@@ -83,6 +83,9 @@ def main():
     ap.add_argument("--pmc-run", action="store_true",
                     help="counter-collection run: the attention kernel 3 times, then a plain "
                          "device copy of COPY_BYTES bytes 3 times (the HBM-counter scale)")
+    ap.add_argument("--pmc-variants", action="store_true",
+                    help="counter-collection run: one launch of the fused kernel per probability "
+                         "stage (EFQ, no-op, exp-then-quantize), bf16 and MXFP8 Q K^T")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -143,6 +146,18 @@ def main():
         attn_ms = [e[1].elapsed_time(e[2]) for e in evs]
         vq_ms = [e[0].elapsed_time(e[1]) for e in evs]
         return total_ms / steps, sum(attn_ms) / steps, sum(vq_ms) / steps, wall
+
+    if args.pmc_variants:
+        qh, kh = binding.quant_qk(q, k, stream=stream)
+        binding.quant_v(v, seq_q=w.seq, heads_q=w.heads_q, out=vhat, stream=stream)
+        for kind in ("efq", "noop", "expq"):
+            prm = binding.PARAMS_MEAN
+            binding.attn_fwd_vhat(q, k, vhat, w.scale, w.causal, kind, prm, out=out, stream=stream)
+            binding.attn_fwd_qk8(qh, kh, vhat, sh, w.scale, w.causal, kind, prm, out=out,
+                                 stream=stream)
+        torch.cuda.synchronize()
+        log(f"[bench] pmc variants done ({w.name})")
+        return
 
     if args.pmc_run:
         binding.quant_v(v, seq_q=w.seq, heads_q=w.heads_q, out=vhat, stream=stream)

@@ -16,6 +16,13 @@ stats TRACE_DIR OUT_FILE COMMAND...
 
 sweep JSONL OUT_FILE COMMAND...
     Table of a `bench.py --sweep` run (one JSON line per sequence length).
+
+counters PMC_DIR OUT_FILE COMMAND...
+    Per attention-kernel variant of a `bench.py --pmc-variants` run with
+    SQ_VALU_MFMA_BUSY_CYCLES, SQ_ACTIVE_INST_VALU, SQ_INSTS_VALU,
+    SQ_INSTS_MFMA and GRBM_GUI_ACTIVE: matrix-core busy and VALU-active
+    cycles per SIMD as fractions of the kernel's cycles, and VALU
+    instructions per SIMD.
 """
 from __future__ import annotations
 
@@ -108,7 +115,45 @@ def sweep(jsonl: str, out: str, command: str):
     print(open(out).read())
 
 
+def counters(d: str, out: str, command: str):
+    import collections
+    rows = []
+    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+        rows += list(csv.DictReader(open(f)))
+    acc = collections.defaultdict(lambda: collections.defaultdict(float))
+    names = {}
+    for r in rows:
+        n = r["Kernel_Name"]
+        if "attn_pp_kernel" not in n:
+            continue
+        key = int(r["Dispatch_Id"])
+        names[key] = n.replace("(anonymous namespace)::", "").replace("void ", "").split("(")[0]
+        acc[key][r["Counter_Name"]] += float(r["Counter_Value"])
+    simds, xcds = 1024, 8
+    with open(out, "w") as fh:
+        fh.write("# matrix-core and VALU activity of the fused attention kernel, qwen3_8b_16k\n")
+        fh.write(f"# command (from the repository root, TMPDIR=/tmp):\n#   {command}\n")
+        fh.write("# kernel template: <head_dim, pgen kind (0 EFQ, 1 EXPQ, 3 no-op), causal, dump, "
+                 "MXFP8 Q K^T>\n")
+        fh.write("# cycles per XCD = GRBM_GUI_ACTIVE / 8; MFMA busy and VALU active are per SIMD "
+                 "(SQ_ACTIVE_INST_VALU is in quad-cycles, summed over the SIMD's waves)\n")
+        fh.write("# kernel | cycles | MFMA busy / cycles | VALU active / cycles | "
+                 "(MFMA + VALU) / cycles | VALU instr per SIMD | MFMA instr per SIMD\n")
+        for key in sorted(acc):
+            c = acc[key]
+            cyc = c["GRBM_GUI_ACTIVE"] / xcds
+            mf = c["SQ_VALU_MFMA_BUSY_CYCLES"] / simds
+            va = 4 * c["SQ_ACTIVE_INST_VALU"] / simds
+            fh.write(f"{names[key]} | {cyc:.0f} | {mf / cyc:.3f} | {va / cyc:.3f} | "
+                     f"{(mf + va) / cyc:.3f} | {c['SQ_INSTS_VALU'] / simds:.0f} | "
+                     f"{c['SQ_INSTS_MFMA'] / simds:.0f}\n")
+    print(open(out).read())
+
+
 def main():
+    if sys.argv[1] == "counters":
+        counters(sys.argv[2], sys.argv[3], " ".join(sys.argv[4:]))
+        return
     if sys.argv[1] == "stats":
         stats(sys.argv[2], sys.argv[3], " ".join(sys.argv[4:]))
         return
