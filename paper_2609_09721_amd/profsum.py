@@ -130,6 +130,8 @@ def counters(d: str, out: str, command: str):
         names[key] = n.replace("(anonymous namespace)::", "").replace("void ", "").split("(")[0]
         acc[key][r["Counter_Name"]] += float(r["Counter_Value"])
     simds, xcds = 1024, 8
+    from paper_2609_09721_amd import inputs
+    pairs = inputs.WORKLOADS["qwen3_8b_16k"].pairs()
     with open(out, "w") as fh:
         fh.write("# matrix-core and VALU activity of the fused attention kernel, qwen3_8b_16k\n")
         fh.write(f"# command (from the repository root, TMPDIR=/tmp):\n#   {command}\n")
@@ -137,8 +139,10 @@ def counters(d: str, out: str, command: str):
                  "MXFP8 Q K^T>\n")
         fh.write("# cycles per XCD = GRBM_GUI_ACTIVE / 8; MFMA busy and VALU active are per SIMD "
                  "(SQ_ACTIVE_INST_VALU is in quad-cycles, summed over the SIMD's waves)\n")
+        fh.write("# VALU per score: wave instructions x 64 lanes / visible (query, key) pairs\n")
         fh.write("# kernel | cycles | MFMA busy / cycles | VALU active / cycles | "
-                 "(MFMA + VALU) / cycles | VALU instr per SIMD | MFMA instr per SIMD\n")
+                 "(MFMA + VALU) / cycles | VALU instr per SIMD | MFMA instr per SIMD | "
+                 "VALU per score\n")
         for key in sorted(acc):
             c = acc[key]
             cyc = c["GRBM_GUI_ACTIVE"] / xcds
@@ -146,7 +150,7 @@ def counters(d: str, out: str, command: str):
             va = 4 * c["SQ_ACTIVE_INST_VALU"] / simds
             fh.write(f"{names[key]} | {cyc:.0f} | {mf / cyc:.3f} | {va / cyc:.3f} | "
                      f"{(mf + va) / cyc:.3f} | {c['SQ_INSTS_VALU'] / simds:.0f} | "
-                     f"{c['SQ_INSTS_MFMA'] / simds:.0f}\n")
+                     f"{c['SQ_INSTS_MFMA'] / simds:.0f} | {c['SQ_INSTS_VALU'] * 64 / pairs:.2f}\n")
     print(open(out).read())
 
 

@@ -87,14 +87,18 @@ def test_pgen_bitexact(B, orc, kind, params):
 
 
 def test_pgen_random_bitexact(B, orc):
+    """1e8 random shifted scores in six chunks of 2^24 (block maxima from 0
+    down to the E8M0 floor, zeros, masked keys), bit-exact."""
     rng = np.random.default_rng(2)
-    x = -rng.exponential(3.0, size=(4096, 512)).astype(np.float32)
-    x[:, ::97] = 0.0
-    xg = torch.from_numpy(x).cuda()
-    cg, eg = B.pgen(xg, "efq")
-    co, eo = orc.pgen(x)
-    assert np.array_equal(eg.cpu().numpy(), eo)
-    assert np.array_equal(unpack(cg.cpu().numpy()), co)
+    for chunk, spread in enumerate([0.5, 1.0, 3.0, 8.0, 30.0, 120.0]):
+        x = -rng.exponential(spread, size=(32768, 512)).astype(np.float32)
+        x[:, ::97] = 0.0
+        if chunk % 2:
+            x[rng.random(x.shape) < 0.05] = -np.inf
+        cg, eg = B.pgen(torch.from_numpy(x).cuda(), "efq")
+        co, eo = orc.pgen(x)
+        assert np.array_equal(eg.cpu().numpy(), eo), chunk
+        assert np.array_equal(unpack(cg.cpu().numpy()), co), chunk
 
 
 @pytest.mark.parametrize("kind", ["expq", "expq6"])
