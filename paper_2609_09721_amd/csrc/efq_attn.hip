@@ -3,11 +3,14 @@
 // Kernels:
 //   vquant_kernel      V (bf16) -> MXFP4 V~ in the FP4 matrix-core operand
 //                      order (HBM-bound pre-pass, once per call).
-//   attn_fwd_kernel    FlashAttention-style forward (Alg. 2 of the paper):
-//                      S^T = K Q^T on bf16 MFMA, the probability stage on the
-//                      VALU (Alg. 1 for EFQ; exp-then-quantize for the
-//                      baseline), O^T += V~^T P~^T on the block-scaled FP4
-//                      MFMA, the denominator P~ 1 from the same operand.
+//   mxfp8_kernel       Q, K (bf16) -> MXFP8 Q^, K^ for the low-bit Q K^T.
+//   attn_pp_kernel     FlashAttention-style forward (Alg. 2 of the paper):
+//                      S^T = K Q^T on bf16 (or block-scaled FP8) MFMA, the
+//                      probability stage on the VALU (Alg. 1 for EFQ;
+//                      exp-then-quantize for the baselines), O^T += V~^T P~^T
+//                      on the block-scaled FP4 MFMA, the denominator P~ 1
+//                      from the same operand; two wave groups alternate
+//                      matrix-core and VALU phases.
 //   pgen_kernel        the probability stage alone on given shifted scores.
 //   pgen_bench_kernel  register-resident throughput probe of that stage.
 //
@@ -48,16 +51,7 @@ constexpr float kLog29 = -1.50407739677627407f;      // log(2/9), Eq. (k-rule)
 constexpr float kLn6 = 1.79175946922805500081f;      // log 6, Eq. (z-def)
 
 constexpr int kWaveQ = 32;     // queries per wave (MFMA N)
-constexpr int kWaves = 4;      // waves per workgroup
-constexpr int kBr = kWaveQ * kWaves;  // queries per workgroup
 constexpr int kBc = 64;        // keys per tile (two 32-key microscaling blocks)
-constexpr int kThreads = 64 * kWaves;
-#ifndef EFQ_PINGPONG
-#define EFQ_PINGPONG 1         // two wave groups in opposite MFMA / VALU phases
-#endif
-#ifndef EFQ_WAVES_PER_SIMD
-#define EFQ_WAVES_PER_SIMD 2   // fused-kernel occupancy target (register budget)
-#endif
 
 // C16 fold table of EFQ-Softmax-LUT (Sec. II-D), nibble j = C16[j].
 constexpr unsigned long long kC16 = 0x7765543322111110ull;
@@ -514,13 +508,11 @@ struct AttnArgs {
 // global_load_lds_dwordx4 (LDS address = base + 16 * lane).  A V~ tile (two
 // 32-key blocks) is stored as in global memory: codes, then E8M0 scales
 // grouped per lane (byte (d % 32) * (D/32) + d / 32 of each block).
-// K and V~ have three buffers each: step j reads K of tile j+1 and V~ of
-// tile j while K of tile j+3 and V~ of tile j+2 stream in, so a load has
-// two steps to land.
-// With MXFP8 Q and K (Q8) a K tile holds E4M3 codes in the order the FP8
-// MFMA reads its A operand (see KLoad8), then 256 bytes of E8M0 scales.
-constexpr int kStages = 3;    // ring depth of the four-wave kernel
-template <int D, int KS = kStages, int VS = kStages, bool Q8 = false>
+// KS K buffers and VS V~ buffers form the LDS rings (depths and schedule
+// at pp_schedule).  With MXFP8 Q and K (Q8) a K tile holds E4M3 codes in the
+// order the FP8 MFMA reads its A operand (see KLoad8), then 256 bytes of
+// E8M0 scales.
+template <int D, int KS, int VS, bool Q8 = false>
 struct Smem {
   static constexpr int kK = Q8 ? kBc * D + 256 : kBc * D * 2;   // one K tile
   static constexpr int kVc = 2 * D * 16;                 // V~ codes of two blocks
@@ -541,7 +533,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, un
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
-template <int D, int NW = kWaves>
+template <int D, int NW>
 struct KLoad {
   static constexpr int KK = D / 16;
   static constexpr int PER = 2 * KK / NW;                // 1 KB blocks per wave
@@ -571,9 +563,10 @@ struct KLoad {
   }
 };
 
-template <int D, int NW = kWaves>
+template <int D, int NW>
 struct VLoad {
-  static constexpr int NB = Smem<D>::kVc / 1024;          // 1 KB code blocks (2 or 4)
+  static constexpr int kVc = Smem<D, 1, 1>::kVc;         // V~ code bytes per tile
+  static constexpr int NB = kVc / 1024;                  // 1 KB code blocks (2 or 4)
   const uint8_t* codes;
   const uint8_t* scales;
   int nb;
@@ -593,7 +586,7 @@ struct VLoad {
     if (wave == NW - 1) {
       // 2 D scale bytes as dwords; for D = 64 the upper lanes repeat the
       // lower ones into the padding
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, vbuf + Smem<D>::kVc, 4, (lane % (2 * D / 4)) * 4,
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, vbuf + kVc, 4, (lane % (2 * D / 4)) * 4,
                                                tile * 2 * D, 0, 0);
     }
   }
@@ -691,32 +684,6 @@ __device__ __forceinline__ void map_work(const AttnArgs& a, int& b, int& hq, int
   b = bh / a.Hq;
 }
 
-// S^T = K Q^T for one 64-key tile (two 32-key windows) from an LDS K tile,
-// with the LDS operand reads issued two steps ahead of their MFMAs.
-template <int D>
-__device__ __forceinline__ void qk_tile(const uint8_t* kbuf, const bf16x8* qreg, int lane,
-                                        f32x16& s0, f32x16& s1) {
-  constexpr int KK = D / 16;
-  const uint8_t* p0 = kbuf + lane * 16;                  // window 0 blocks
-  const uint8_t* p1 = p0 + KK * 1024;                    // window 1 blocks
-  bf16x8 a0[2], a1[2];
-  a0[0] = *(const bf16x8*)(p0);
-  a1[0] = *(const bf16x8*)(p1);
-  a0[1] = *(const bf16x8*)(p0 + 1024);
-  a1[1] = *(const bf16x8*)(p1 + 1024);
-  s0 = f32x16{};
-  s1 = f32x16{};
-#pragma unroll
-  for (int kk = 0; kk < KK; ++kk) {
-    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[kk & 1], qreg[kk], s0, 0, 0, 0);
-    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[kk & 1], qreg[kk], s1, 0, 0, 0);
-    if (kk + 2 < KK) {
-      a0[kk & 1] = *(const bf16x8*)(p0 + (kk + 2) * 1024);
-      a1[kk & 1] = *(const bf16x8*)(p1 + (kk + 2) * 1024);
-    }
-  }
-}
-
 // V~ operands of one tile for the lane: the 16 code bytes of each slab and
 // the E8M0 scales of all slabs in one register (slab s = byte s).
 template <int D>
@@ -732,7 +699,7 @@ __device__ __forceinline__ void read_v(const uint8_t* vb, int lane, VOps<D>& v) 
   const uint8_t* vc = vb + (half * D + (lane & 31)) * 16;
 #pragma unroll
   for (int s = 0; s < NS; ++s) v.a[s] = *(const u32x4*)(vc + s * 32 * 16);
-  const uint8_t* vsp = vb + Smem<D>::kVc + half * D + (lane & 31) * NS;
+  const uint8_t* vsp = vb + Smem<D, 1, 1>::kVc + half * D + (lane & 31) * NS;
   if constexpr (NS == 4) v.sv = *(const int*)vsp;
   else v.sv = *(const unsigned short*)vsp;
 }
@@ -758,259 +725,6 @@ __device__ __forceinline__ void mask_tile(f32x16& s0, f32x16& s1, int lim, int h
     const int kofs = 8 * (r >> 2) + (r & 3);
     s0[r] = kofs < l0 ? s0[r] : -INFINITY;
     s1[r] = kofs + 32 < l0 ? s1[r] : -INFINITY;
-  }
-}
-
-// History rescale A *= alpha, l *= alpha, skipped (a uniform branch) on
-// tiles where no row maximum of the wave moved (alpha = 1 on all lanes).
-template <int NS>
-__device__ __forceinline__ void rescale(f32x16* oacc, f32x16& lacc, float alpha) {
-  if (__builtin_amdgcn_ballot_w64(alpha != 1.0f) != 0ull) {
-#pragma unroll
-    for (int s = 0; s < NS; ++s) oacc[s] *= alpha;
-    lacc[0] *= alpha;
-  }
-}
-
-
-// Regions 1 .. KK-1 of the pipelined step (see step_next).
-template <int D, int KIND, int I>
-__device__ __forceinline__ void qk_regions(const uint8_t* p0, const uint8_t* p1, bf16x8* a0,
-                                           bf16x8* a1, const bf16x8* qreg, f32x16& sn0,
-                                           f32x16& sn1, const uint8_t* vb, int lane, VOps<D>& vop,
-                                           const f32x16& sc0, const f32x16& sc1,
-                                           const PgenArgs& pa, PgenState& st) {
-  constexpr int KK = D / 16;
-  if constexpr (I < KK) {
-    sn0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[I & 1], qreg[I], sn0, 0, 0, 0);
-    sn1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[I & 1], qreg[I], sn1, 0, 0, 0);
-    if constexpr (I + 2 < KK) {
-      a0[I & 1] = *(const bf16x8*)(p0 + (I + 2) * 1024);
-      a1[I & 1] = *(const bf16x8*)(p1 + (I + 2) * 1024);
-    }
-    if constexpr (I == KK - 1) read_v<D>(vb, lane, vop);
-    constexpr int P0 = 16 * (I - 1) / (KK - 1), P1 = 16 * I / (KK - 1);
-    pg_pairs<KIND, 2 * P0, 2 * P1>(sc0, sc1, pa, st);
-    __builtin_amdgcn_sched_barrier(0);
-    qk_regions<D, KIND, I + 1>(p0, p1, a0, a1, qreg, sn0, sn1, vb, lane, vop, sc0, sc1, pa, st);
-  }
-}
-
-// One software-pipelined step: the probability stage of tile j (scores sc)
-// interleaved, region by region, with S(j+1) = K(j+1) Q^T on the bf16 MFMA.
-// Each region holds one k-step (two MFMAs), the LDS operand reads of the
-// k-step two ahead, and a slice of VALU work; sched_barrier keeps the
-// regions in this order.  The V~ operands of tile j are read in the last
-// region (into the freed operand registers).
-template <int D, int KIND>
-__device__ __forceinline__ PgenOut step_next(const uint8_t* kb_next, const uint8_t* vb, const bf16x8* qreg,
-                                             int lane, const f32x16& sc0, const f32x16& sc1,
-                                             f32x16& sn0, f32x16& sn1, float& m, const PgenArgs& pa,
-                                             VOps<D>& vop) {
-  constexpr int KK = D / 16;
-  const uint8_t* p0 = kb_next + lane * 16;     // window 0 operand blocks
-  const uint8_t* p1 = p0 + KK * 1024;          // window 1 operand blocks
-  bf16x8 a0[2], a1[2];
-  PgenState st;
-  float pm0, pm1;
-
-  a0[0] = *(const bf16x8*)(p0);
-  a1[0] = *(const bf16x8*)(p1);
-  a0[1] = *(const bf16x8*)(p0 + 1024);
-  a1[1] = *(const bf16x8*)(p1 + 1024);
-  pg_max<KIND>(sc0, sc1, pm0, pm1);
-  __builtin_amdgcn_sched_barrier(0);
-
-  sn0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[0], qreg[0], f32x16{}, 0, 0, 0);
-  sn1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[0], qreg[0], f32x16{}, 0, 0, 0);
-  if constexpr (KK > 2) {
-    a0[0] = *(const bf16x8*)(p0 + 2 * 1024);
-    a1[0] = *(const bf16x8*)(p1 + 2 * 1024);
-  }
-  pg_params<KIND>(pm0, pm1, m, pa, st);
-  __builtin_amdgcn_sched_barrier(0);
-
-  qk_regions<D, KIND, 1>(p0, p1, a0, a1, qreg, sn0, sn1, vb, lane, vop, sc0, sc1, pa, st);
-  if constexpr (KIND == EFQ_PGEN_NOOP) asm volatile("" ::"v"(sc0), "v"(sc1));
-  return pg_finish<KIND>(st);
-}
-
-// Per-wave state of the fused kernel and one pipeline step.
-template <int D, int KIND, bool DUMP>
-struct WaveCtx {
-  static constexpr int NS = D / 32;   // 32-row slabs of O^T
-  bf16x8 qreg[D / 16];                // Q^T operand (lane: query my_q)
-  f32x16 oacc[NS];                    // O^T accumulators
-  f32x16 lacc;                        // row 0 carries l (P~ 1 on the MFMA)
-  float m;                            // running maximum
-  PgenArgs pa;
-  int lane, half, my_q, vis_end;
-
-  // Step j: the probability stage of tile j (scores c0, c1), the history
-  // rescale, and O^T += V~^T P~^T, l += P~ 1.  With NEXT, S(j+1) = K(j+1)
-  // Q^T is computed into n0, n1 in the same pass, interleaved region by
-  // region with the VALU work.
-  template <bool NEXT>
-  __device__ __forceinline__ void step(int j, const uint8_t* kbuf0, const uint8_t* vbuf0,
-                                       const AttnArgs& a, int b, int hq, const f32x16& c0,
-                                       const f32x16& c1, f32x16& n0, f32x16& n1) {
-    const uint8_t* vb = vbuf0 + (j % kStages) * Smem<D>::kV;
-    VOps<D> vop;
-    PgenOut po;
-    if constexpr (NEXT) {
-      po = step_next<D, KIND>(kbuf0 + ((j + 1) % kStages) * Smem<D>::kK, vb, qreg, lane, c0, c1,
-                              n0, n1, m, pa, vop);
-    } else {
-      read_v<D>(vb, lane, vop);
-      po = pgen<KIND>(c0, c1, m, pa);
-    }
-
-    if constexpr (DUMP) {
-      const int blk = 2 * j + half;
-      if (my_q < a.Sq && blk < a.nblk) {
-        long row = ((long)b * a.Hq + hq) * a.Sq + my_q;
-        *(u32x4*)(a.p_codes + (row * a.nblk + blk) * 16) = unpermute_codes(po.bop);
-        a.p_e8m0[row * a.nblk + blk] = (uint8_t)po.scale_b;
-      }
-    }
-
-    // ---- rescale history when a row maximum moved (alpha = 1 otherwise)
-    rescale<NS>(oacc, lacc, po.alpha);
-
-    // ---- O^T += V~^T P~^T and l += P~ 1 on the FP4 MFMA (all-ones A, 2^0)
-    const i32x8 bop = i32x8{(int)po.bop[0], (int)po.bop[1], (int)po.bop[2], (int)po.bop[3], 0, 0, 0, 0};
-    pv_slabs<NS>(oacc, vop, bop, po.scale_b);
-    const i32x8 ones = i32x8{0x22222222, 0x22222222, 0x22222222, 0x22222222, 0, 0, 0, 0};
-    lacc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ones, bop, lacc, 4, 4, 0, 127, 0,
-                                                           po.scale_b);
-    if constexpr (NEXT) {
-      const int lim = vis_end - (j + 1) * kBc;
-      if (lim < kBc) mask_tile(n0, n1, lim, half);
-    }
-  }
-};
-
-template <int D, int KIND, bool CAUSAL, bool DUMP>
-__global__ __launch_bounds__(kThreads, EFQ_WAVES_PER_SIMD) void attn_fwd_kernel(
-    const unsigned short* __restrict__ q, const unsigned short* __restrict__ k,
-    const uint8_t* __restrict__ vhat, float* __restrict__ out, AttnArgs a) {
-  extern __shared__ __align__(16) uint8_t smem[];
-  constexpr int KK = D / 16;   // k-steps of the Q K^T MFMA
-  constexpr int NS = D / 32;   // 32-row slabs of O^T
-
-  int b, hq, qt;
-  map_work(a, b, hq, qt);
-  const int g = hq / (a.Hq / a.Hkv);
-  const int wave = threadIdx.x >> 6;
-  WaveCtx<D, KIND, DUMP> w;
-  w.lane = threadIdx.x & 63;
-  w.half = w.lane >> 5;
-  const int q_wave0 = qt * kBr + wave * kWaveQ;
-  w.my_q = q_wave0 + (w.lane & 31);
-  const int q_load = w.my_q < a.Sq ? w.my_q : a.Sq - 1;
-
-  // Q^T operand in registers: lane holds Q[my_q][kk*16 + half*8 .. +8]
-  {
-    const unsigned short* qp = q + (((long)b * a.Sq + q_load) * a.Hq + hq) * D + w.half * 8;
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) w.qreg[kk] = *(const bf16x8*)(qp + kk * 16);
-  }
-
-  const int kv_end = CAUSAL ? min(a.Sk, qt * kBr + kBr) : a.Sk;
-  const int wave_end = CAUSAL ? min(a.Sk, q_wave0 + kWaveQ) : a.Sk;
-  const int ntiles = (kv_end + kBc - 1) / kBc;         // workgroup
-  const int wtiles = (wave_end + kBc - 1) / kBc;        // this wave
-  // visible keys of this lane: [0, vis_end)
-  w.vis_end = CAUSAL ? min(a.Sk, w.my_q + 1) : a.Sk;
-
-  KLoad<D> kload;
-  kload.init(k + (long)b * a.Sk * a.Hkv * D, a.Sk, a.Hkv, g, wave, w.lane);
-  VLoad<D> vload;
-  vload.init(vhat + ((long)b * a.Hkv + g) * a.nb * D * 16,
-             vhat + a.scale_off + ((long)b * a.Hkv + g) * a.nb * D, a.nb);
-  uint8_t* const kbuf0 = smem + Smem<D>::kKOff;
-  uint8_t* const vbuf0 = smem + Smem<D>::kVOff;
-  const int v_issued = VLoad<D>::issued(wave);
-
-  w.pa.scale = a.scale;
-  w.pa.sh = a.scale * a.h;
-  w.pa.sh32 = 32.0f * w.pa.sh;
-  w.pa.c = kLn6 + a.tau;
-  w.pa.negh = -a.h;
-  w.pa.l2s = a.scale * kInvLn2;
-#pragma unroll
-  for (int s = 0; s < NS; ++s) w.oacc[s] = f32x16{};
-  w.lacc = f32x16{};
-  w.m = -INFINITY;
-
-  // prologue: K(0) V~(0) K(1) | V~(1) K(2) in flight; S(0)
-  kload.issue(kbuf0, 0, wave);
-  vload.issue(vbuf0, 0, wave, w.lane);
-  int late = 0;
-  if (ntiles > 1) {
-    kload.issue(kbuf0 + Smem<D>::kK, 1, wave);
-    vload.issue(vbuf0 + Smem<D>::kV, 1, wave, w.lane);
-    late += v_issued;
-  }
-  if (ntiles > 2) {
-    kload.issue(kbuf0 + 2 * Smem<D>::kK, 2, wave);
-    late += KLoad<D>::kIssued;
-  }
-  wait_vmem_le(late);
-  __syncthreads();
-  f32x16 sa0, sa1, sb0, sb1;
-  if (wtiles > 0) {
-    qk_tile<D>(kbuf0, w.qreg, w.lane, sa0, sa1);
-    if (w.vis_end < kBc) mask_tile(sa0, sa1, w.vis_end, w.half);
-  }
-
-  // One step: wait for the tile of the previous step's loads, publish it,
-  // stream K(j+3) and V~(j+2), compute.  Scores ping-pong between two
-  // register sets (two steps per loop trip) instead of being copied.
-  auto one = [&](int j, const f32x16& c0, const f32x16& c1, f32x16& n0, f32x16& n1) {
-    __syncthreads();
-    int issued = 0;
-    if (j + 3 < ntiles) {
-      kload.issue(kbuf0 + (j % kStages) * Smem<D>::kK, j + 3, wave);
-      issued += KLoad<D>::kIssued;
-    }
-    if (j + 2 < ntiles) {
-      vload.issue(vbuf0 + ((j + 2) % kStages) * Smem<D>::kV, j + 2, wave, w.lane);
-      issued += v_issued;
-    }
-    if (j + 1 < wtiles)
-      w.template step<true>(j, kbuf0, vbuf0, a, b, hq, c0, c1, n0, n1);
-    else if (j < wtiles)
-      w.template step<false>(j, kbuf0, vbuf0, a, b, hq, c0, c1, n0, n1);
-    wait_vmem_le(issued);   // everything but this step's own loads has landed
-  };
-  for (int j = 0; j < ntiles; j += 2) {
-    one(j, sa0, sa1, sb0, sb1);
-    if (j + 1 < ntiles) one(j + 1, sb0, sb1, sa0, sa1);
-  }
-
-  // ---- O = A / l, fp32 store; lane holds query my_q, rows d of each slab
-  const float l = w.lacc[0];
-  const float rl = 1.0f / l;   // one division per row, then multiplies
-  if (w.my_q < a.Sq) {
-    float* op = out + (((long)b * a.Sq + w.my_q) * a.Hq + hq) * D;
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-#pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        int d = s * 32 + 8 * r4 + 4 * w.half;
-        f32x4 v4 = f32x4{w.oacc[s][4 * r4] * rl, w.oacc[s][4 * r4 + 1] * rl,
-                         w.oacc[s][4 * r4 + 2] * rl, w.oacc[s][4 * r4 + 3] * rl};
-        *(f32x4*)(op + d) = v4;
-      }
-    }
-    if constexpr (DUMP) {
-      long row = ((long)b * a.Hq + hq) * a.Sq + w.my_q;
-      if (w.half == 0) {
-        a.row_m[row] = is_expq<KIND>() ? w.m * kLn2 : w.m;
-        a.row_l[row] = l;
-      }
-    }
   }
 }
 
@@ -1692,11 +1406,7 @@ __global__ __launch_bounds__(256) void rho_final_kernel(const double* __restrict
 }
 
 // ================================================================ host side
-#if EFQ_PINGPONG
 constexpr int kQTile = kPPBr;   // queries per workgroup of the launched kernel
-#else
-constexpr int kQTile = kBr;
-#endif
 
 thread_local char g_msg[512] = "ok";
 
@@ -1787,7 +1497,6 @@ int launch_vquant(const void* v, const efq_shape* s, void* vhat, hipStream_t st)
 template <int D, int KIND, bool CAUSAL, bool DUMP, bool Q8>
 hipError_t launch_attn_t(const void* q, const void* k, const void* vhat, float* out,
                          const AttnArgs& a, hipStream_t st, unsigned grid) {
-#if EFQ_PINGPONG
   // more dynamic LDS than the default limit: raise it once per kernel (the
   // call is idempotent, so a race between threads is harmless)
   static bool lds_ok = false;
@@ -1801,12 +1510,6 @@ hipError_t launch_attn_t(const void* q, const void* k, const void* vhat, float* 
   constexpr int lds = SmemPP<D, Q8>::kTotal;
   hipLaunchKernelGGL((attn_pp_kernel<D, KIND, CAUSAL, DUMP, Q8>), dim3(grid), dim3(kPPThreads),
                      lds, st, q, k, (const uint8_t*)vhat, out, a);
-#else
-  if constexpr (Q8) return hipErrorNotSupported;
-  hipLaunchKernelGGL((attn_fwd_kernel<D, KIND, CAUSAL, DUMP>), dim3(grid), dim3(kThreads),
-                     Smem<D>::kTotal, st, (const unsigned short*)q, (const unsigned short*)k,
-                     (const uint8_t*)vhat, out, a);
-#endif
   return hipGetLastError();
 }
 
