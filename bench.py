@@ -16,6 +16,8 @@ Besides the headline TFLOP/s it reports
   * lowbit: the low-bit variant (MXFP8 Q and K, Q K^T on the FP8 matrix
     core) on the same workload, its fused kernel against the FP8 / MXFP4
     peaks, per probability stage;
+  * target and workloads: the fused kernel on the other benchmark shapes
+    (Qwen3-8B 32K and 128K, Qwen3-VL 32K, WAN2.2 75600);
   * cpu_baseline: the CPU oracle on a bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -264,6 +266,9 @@ def main():
     if not args.no_extra and args.target_workload:
         result["target"] = target_run(args, binding, inputs, dev, stream)
 
+    if not args.no_extra:
+        result["workloads"] = workloads_run(binding, inputs, dev, stream)
+
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(w, q, k, v, args.cpu_seconds)
 
@@ -402,6 +407,45 @@ def lowbit_run(w, binding, q, k, v, vhat, out, stream, steps):
     res["step_ms"] = round(ms, 4)
     res["step_tflops"] = round(w.flops() / (ms * 1e-3) / 1e12, 2)
     del qh, kh, ws
+    return res
+
+
+def workloads_run(binding, inputs, dev, stream):
+    """The other benchmark shapes (Qwen3-8B 128K causal, Qwen3-VL 32K and
+    WAN2.2 75600 non-causal): fused-kernel time (median of 3 launches) per
+    probability stage, bf16 and MXFP8 Q K^T, and the fraction of each
+    path's MFMA roofline."""
+    import torch
+    peak = 1.0 / (0.5 / PEAK_BF16 + 0.5 / PEAK_FP4)
+    peak8 = 1.0 / (0.5 / PEAK_FP8 + 0.5 / PEAK_FP4)
+    res = {"timing": "median of 3 launches after one warm-up"}
+    for name in ("qwen3_8b_128k", "qwen3_vl_32k", "wan22_75600"):
+        w = inputs.WORKLOADS[name]
+        q, k, v = inputs.make_qkv(w, device=dev)
+        vh = binding.quant_v(v, seq_q=w.seq, heads_q=w.heads_q, stream=stream)
+        qh, kh = binding.quant_qk(q, k, stream=stream)
+        sh = binding.shape_of(q, k)
+        out = torch.empty(q.shape, dtype=torch.float32, device=dev)
+        r = {"batch": w.batch, "heads_q": w.heads_q, "heads_kv": w.heads_kv, "seq": w.seq,
+             "causal": w.causal, "flops": w.flops()}
+        for kind in ("efq", "expq"):
+            def call(kind=kind):
+                binding.attn_fwd_vhat(q, k, vh, w.scale, w.causal, kind, binding.PARAMS_MEAN,
+                                      out=out, stream=stream)
+
+            def call8(kind=kind):
+                binding.attn_fwd_qk8(qh, kh, vh, sh, w.scale, w.causal, kind, binding.PARAMS_MEAN,
+                                     out=out, stream=stream)
+            for fn, key, pk in ((call, kind, peak), (call8, "lowbit_" + kind, peak8)):
+                fn()
+                torch.cuda.synchronize()
+                ms = _median_call(fn, 3, stream)
+                tf = w.flops() / (ms * 1e-3) / 1e12
+                r[key] = {"attn_ms": round(ms, 3), "tflops": round(tf, 1), "frac": round(tf / pk, 4)}
+        res[name] = r
+        log(f"[bench] {name}: efq {r['efq']['attn_ms']} ms, low-bit efq {r['lowbit_efq']['attn_ms']} ms")
+        del q, k, v, vh, qh, kh, out
+        torch.cuda.empty_cache()
     return res
 
 

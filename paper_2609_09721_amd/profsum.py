@@ -20,9 +20,10 @@ sweep JSONL OUT_FILE COMMAND...
 counters PMC_DIR OUT_FILE COMMAND...
     Per attention-kernel variant of a `bench.py --pmc-variants` run with
     SQ_VALU_MFMA_BUSY_CYCLES, SQ_ACTIVE_INST_VALU, SQ_INSTS_VALU,
-    SQ_INSTS_MFMA and GRBM_GUI_ACTIVE: matrix-core busy and VALU-active
-    cycles per SIMD as fractions of the kernel's cycles, and VALU
-    instructions per SIMD.
+    SQ_INSTS_MFMA, SQ_INSTS_LDS, SQ_LDS_BANK_CONFLICT and GRBM_GUI_ACTIVE:
+    matrix-core busy and VALU-active cycles per SIMD as fractions of the
+    kernel's cycles, VALU instructions per SIMD and per score, and LDS
+    bank-conflict stall cycles per LDS instruction.
 """
 from __future__ import annotations
 
@@ -142,7 +143,7 @@ def counters(d: str, out: str, command: str):
         fh.write("# VALU per score: wave instructions x 64 lanes / visible (query, key) pairs\n")
         fh.write("# kernel | cycles | MFMA busy / cycles | VALU active / cycles | "
                  "(MFMA + VALU) / cycles | VALU instr per SIMD | MFMA instr per SIMD | "
-                 "VALU per score\n")
+                 "VALU per score | LDS instr per SIMD | bank-conflict cycles per LDS instr\n")
         for key in sorted(acc):
             c = acc[key]
             cyc = c["GRBM_GUI_ACTIVE"] / xcds
@@ -150,7 +151,9 @@ def counters(d: str, out: str, command: str):
             va = 4 * c["SQ_ACTIVE_INST_VALU"] / simds
             fh.write(f"{names[key]} | {cyc:.0f} | {mf / cyc:.3f} | {va / cyc:.3f} | "
                      f"{(mf + va) / cyc:.3f} | {c['SQ_INSTS_VALU'] / simds:.0f} | "
-                     f"{c['SQ_INSTS_MFMA'] / simds:.0f} | {c['SQ_INSTS_VALU'] * 64 / pairs:.2f}\n")
+                     f"{c['SQ_INSTS_MFMA'] / simds:.0f} | {c['SQ_INSTS_VALU'] * 64 / pairs:.2f} | "
+                     f"{c.get('SQ_INSTS_LDS', 0) / simds:.0f} | "
+                     f"{c.get('SQ_LDS_BANK_CONFLICT', 0) / max(c.get('SQ_INSTS_LDS', 0), 1):.4f}\n")
     print(open(out).read())
 
 
