@@ -31,8 +31,10 @@
  *    stream) and never synchronise the host (efq_calibrate excepted).  The
  *    caller owns every buffer;
  *    the library keeps no allocation beyond its code objects, except that the
- *    convenience entry points without a workspace argument take one
- *    stream-ordered allocation for V~ and release it on the same stream.
+ *    convenience entry points without a workspace argument (and the _ex,
+ *    lowbit_ex and calibrate entry points when given no workspace) take one
+ *    stream-ordered allocation for their scratch (V~; Q^, K^ and V~; the
+ *    calibration buffers) and release it on the same stream.
  *  - Every argument is validated before any HIP call: on error nothing is
  *    enqueued and a negative status is returned.  A failed launch returns
  *    EFQ_EHIP.  efq_strerror() gives a thread-local message for the last
