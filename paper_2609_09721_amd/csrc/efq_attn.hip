@@ -752,6 +752,23 @@ constexpr int kPPThreads = 64 * kPPWaves;
 constexpr int kPP = EFQ_PREFETCH;          // tiles streamed ahead (>= 2)
 constexpr int kPPK = kPP + 1;              // K ring depth
 constexpr int kPPV = kPP + 2;              // V~ ring depth
+// Wave priorities (s_setprio) of the two phases, per probability stage: the
+// issue arbiter of a SIMD favours the wave whose work is on the critical
+// path.  EFQ: the VALU phase (max, parameters, rescale) is the longer one;
+// exp-then-quantize and LUT: the matrix phase carries their heavier code
+// step.  Measured, not derived (both orders were timed).
+#ifndef EFQ_PRIO_EFQ_M
+#define EFQ_PRIO_EFQ_M 0
+#endif
+#ifndef EFQ_PRIO_EFQ_V
+#define EFQ_PRIO_EFQ_V 3
+#endif
+#ifndef EFQ_PRIO_OTHER_M
+#define EFQ_PRIO_OTHER_M 3
+#endif
+#ifndef EFQ_PRIO_OTHER_V
+#define EFQ_PRIO_OTHER_V 0
+#endif
 #ifndef EFQ_KPRE_BF16
 #define EFQ_KPRE_BF16 0                    // also on the bf16 Q K^T path
 #endif
@@ -996,6 +1013,10 @@ struct PPWave {
   int lane, half, my_q, vis_end;
   // the pre-read needs registers the bf16 exp-then-quantize variants lack
   static constexpr bool kPreOn = kKPre && (Q8 || EFQ_KPRE_BF16);
+  static constexpr int kMPrio = KIND == EFQ_PGEN_EFQ ? EFQ_PRIO_EFQ_M
+                                : KIND == EFQ_PGEN_NOOP ? 0 : EFQ_PRIO_OTHER_M;
+  static constexpr int kVPrio = KIND == EFQ_PGEN_EFQ ? EFQ_PRIO_EFQ_V
+                                : KIND == EFQ_PGEN_NOOP ? 0 : EFQ_PRIO_OTHER_V;
 
   // Matrix phase M(j): with QK the scores of tile j into sn, and with CODES
   // the codes of tile j-1 (scores sc) in the shadow of those MFMAs, then its
@@ -1005,6 +1026,7 @@ struct PPWave {
                                          const KPre<D, Q8>& kp, const AttnArgs& a, int b, int hq,
                                          f32x16& sn0, f32x16& sn1, const f32x16& sc0,
                                          const f32x16& sc1) {
+    if constexpr (kMPrio != kVPrio) __builtin_amdgcn_s_setprio(kMPrio);
     const uint8_t* kb = kbuf0 + ((QK ? j : 0) % kPPK) * SmemPP<D, Q8>::kK;
     constexpr bool P = PRE && kPreOn;
     PgenOut po;
@@ -1036,6 +1058,7 @@ struct PPWave {
   // operands stay in registers.
   __device__ __forceinline__ void vphase(int j, const uint8_t* vbuf0, const uint8_t* kbuf0,
                                          f32x16& s0, f32x16& s1, VOps<D>& vop, KPre<D, Q8>& kp) {
+    if constexpr (kMPrio != kVPrio) __builtin_amdgcn_s_setprio(kVPrio);
     if constexpr (kPreOn) kp.read(kbuf0 + ((j + 1) % kPPK) * SmemPP<D, Q8>::kK, lane);
     read_v<D>(vbuf0 + (j % kPPV) * SmemPP<D, Q8>::kV, lane, vop);
     const int lim = vis_end - j * kBc;
