@@ -50,12 +50,14 @@
  *             ~ 32 (u_t + 1) - 1/2,  u_t = (x_t - k_b log2 - log6 - tau) h
  *                                        = (z_t - tau) h      Eq. (d8-index)
  *         c_t = floor(min(max(rne(w_t), 0), 255) / 32)
- *   LUT:  u_t = fma(acc_t, fl(scale*h), B),  j16 = clip(floor(u_t) + 1, 0, 15)
+ *   LUT:  w_t = fma(acc_t, 16 fl(scale*h), fl(16 B + 15.5)) ~ 16 (u_t + 1) - 1/2
+ *         j16 = floor(min(max(rne(w_t), 0), 255) / 16),  c_t = C16[j16]
  *
  * In exact arithmetic floor(min(max(rne(32 v - 1/2), 0), 255) / 32) is
  * clip(floor(v), 0, 7) for every real v (a half-integer 32 n - 1/2 rounds
  * to the even 32 n, and 32 n + 31.5 only occurs at v = n + 1), so c_t is
- * clip(floor(u_t) + 1, 0, 7) of Eq. (d8-index).  The residual argument is
+ * clip(floor(u_t) + 1, 0, 7) of Eq. (d8-index).  With 16 in place of 32 the
+ * same argument gives j16 = clip(floor(u_t) + 1, 0, 15) for the LUT index.  The residual argument is
  * one fused multiply-add of the raw dot product with the row and block
  * terms folded into a bias; in fp32 it can differ from a step-by-step
  * evaluation only within a few ulps of a code threshold.  orc_pgen_real
@@ -111,15 +113,16 @@ static int code_from_w(float w)
     return (int)r / 32;
 }
 
-/* floor(u) + 1 clipped to [0, top]; u = -inf or below gives 0. */
-static int affine_index(float u, int top)
+/* LUT index from w ~ 16 (u + 1) - 1/2: round to nearest (ties to even),
+ * saturate to [0, 255], keep the multiple of 16.  -inf and NaN give 0. */
+static int index_from_w16(float w)
 {
-    float fu = floorf(u);
-    if (!(fu >= -1.0f)) /* also catches -inf */
+    float r = nearbyintf(w);
+    if (!(r > 0.0f))
         return 0;
-    if (fu >= (float)top)
-        return top;
-    return (int)fu + 1;
+    if (r > 255.0f)
+        r = 255.0f;
+    return (int)r / 16;
 }
 
 /* Nearest E2M1 magnitude code for y >= 0 among C8, ties to the even code
@@ -160,7 +163,7 @@ static int floor_log2(double a)
  * Diagnostic (margin != NULL): lowers *margin to the smallest distance, in
  * units of the raw dot product, between an argument of this block's
  * decisions and the nearest value where that decision changes (k_b at
- * integer q, an EFQ code at w = 32 n - 1/2, a LUT index at integer u).  It
+ * integer q, an EFQ code at w = 32 n - 1/2, a LUT index at w = 16 n - 1/2).  It
  * does not change any result; a check that compares against an
  * implementation whose dot products differ in the last bits uses it to
  * tell a legitimate code flip from an error.
@@ -201,8 +204,9 @@ static int pgen_block(const float *acc, int n, float scale, float m, float tau,
      * c_t = clip(floor((z_t - tau) h) + 1, 0, 7) (Eq. d8-index), or for the
      * LUT variant j16 = clip(floor((z_t - tau16) h16) + 1, 0, 15), c_t = C16[j16].
      * (z_t - tau) h is evaluated as acc_t (scale h) - (m + k_b log2 + log6 + tau) h;
-     * for EFQ the floor, the +1 and both clips come from rounding
-     * 32 ((z_t - tau) h + 1) - 1/2 to an integer in [0, 255] (header). */
+     * the floor, the +1 and both clips come from rounding
+     * 32 ((z_t - tau) h + 1) - 1/2 (EFQ; 16 (...) - 1/2 for the LUT index) to an
+     * integer in [0, 255] (header). */
     float kf = (float)k;
     float klog2 = kf * F_LN2;
     float c0 = F_LN6 + tau;
@@ -212,18 +216,20 @@ static int pgen_block(const float *acc, int n, float scale, float m, float tau,
     float sh = scale * h;
     float sh32 = 32.0f * sh;                  /* exact */
     float bias32 = fmaf(bias, 32.0f, 31.5f);  /* fl(32 B + 31.5) */
+    float sh16 = 16.0f * sh;                  /* exact */
+    float bias16 = fmaf(bias, 16.0f, 15.5f);  /* fl(16 B + 15.5) */
     for (int t = 0; t < n; ++t) {
         if (acc[t] == -INFINITY) {
             codes[t] = 0;
             continue;
         }
         if (lut) {
-            float u = fmaf(acc[t], sh, bias);
-            codes[t] = (uint8_t)C16[affine_index(u, 15)];
+            float w = fmaf(acc[t], sh16, bias16);
+            codes[t] = (uint8_t)C16[index_from_w16(w)];
             if (margin) {
-                double nb = nearbyint((double)u);
-                nb = nb < 0.0 ? 0.0 : (nb > 14.0 ? 14.0 : nb);
-                double d = fabs((double)u - nb) / (double)sh;
+                double nb = nearbyint(((double)w + 0.5) / 16.0);
+                nb = nb < 1.0 ? 1.0 : (nb > 15.0 ? 15.0 : nb);
+                double d = fabs((double)w - (16.0 * nb - 0.5)) / (double)sh16;
                 if (d < *margin)
                     *margin = d;
             }

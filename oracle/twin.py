@@ -71,9 +71,12 @@ def pgen_fp32(x: np.ndarray, tau: float, h: float, lut: bool = False,
     bias = -((m + off) * h)
     acc = np.where(masked, F32(0), xp)
     if lut:
-        u = fma32(acc, F32(scale * h), bias[:, :, None])
-        fu = np.floor(u.astype(np.float64))
-        j = np.clip(fu + 1, 0, 15).astype(np.int64)
+        # w ~ 16 (u + 1) - 1/2, nearest-even, saturate, multiple of 16:
+        # clip(floor(u) + 1, 0, 15)
+        bias16 = fma32(bias, F32(16.0), F32(15.5))
+        w = fma32(acc, F32(16.0) * F32(scale * h), bias16[:, :, None])
+        r = np.rint(w.astype(np.float64))
+        j = (np.clip(r, 0, 255) // 16).astype(np.int64)
         c = C16[j]
     else:
         # w ~ 32 (u + 1) - 1/2; nearest-even to an integer, saturate to

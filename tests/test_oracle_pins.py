@@ -146,6 +146,49 @@ def test_code_flips_at_threshold(orc):
         assert abs(hi - xt) < 2e-6, (c, hi, xt)
 
 
+def test_lut_matches_index_threshold_form(orc):
+    """Sec. II-D: the LUT index j16 counts the thresholds tau16 + (j-1)/h16
+    (j = 1..15) at or below z, and the code is C16[j16] (the printed table)."""
+    g = golden_constants()
+    tau16 = math.log(g["lut_tau_num"][0] / g["lut_tau_den"][0])
+    h16 = g["lut_h_num"][0] / math.log(g["lut_h_logarg"][0])
+    c16 = np.array([int(v) for v in g["c16"]])
+    rng = np.random.default_rng(31)
+    n = 4000
+    x = np.zeros((n, 32), np.float32)            # block maximum 0: k = -3
+    x[:, 1:] = -rng.uniform(0, 6, size=(n, 31)).astype(np.float32)
+    codes, e8 = orc.pgen(x, orc.LUT_MODE, *orc.LUT)
+    assert np.all(e8 == 124)
+    z = x.astype(np.float64) + 3 * LN2 - LN6
+    thr = tau16 + np.arange(0, 15) / h16
+    j16 = (z[..., None] >= thr).sum(-1)
+    near = np.min(np.abs(z[..., None] - thr), axis=-1) < 1e-5
+    assert near.mean() < 1e-3
+    assert np.array_equal(codes[~near], c16[j16][~near])
+
+
+def test_lut_index_steps_at_threshold(orc):
+    """Bisect the oracle's LUT decision in x: the index (so the code, where
+    C16 steps) changes at z = tau16 + j/h16."""
+    tau16, h16 = orc.LUT
+    c16 = list(orc.C16)
+    for j in range(15):
+        if c16[j] == c16[j + 1]:
+            continue
+        xt = tau16 + j / h16 - 3 * LN2 + LN6
+        lo, hi = xt - 1e-3, xt + 1e-3
+        for _ in range(40):
+            mid = np.float32((lo + hi) / 2)
+            x = np.full((1, 32), -np.inf, np.float32)
+            x[0, 0], x[0, 1] = 0.0, mid
+            codes, _ = orc.pgen(x, orc.LUT_MODE, tau16, h16)
+            if codes[0, 1] > c16[j]:
+                hi = float(mid)
+            else:
+                lo = float(mid)
+        assert abs(hi - xt) < 2e-6, (j, hi, xt)
+
+
 def test_format_and_nonnegativity(orc):
     """Codes are non-negative E2M1 patterns 0..7; E8M0 = k + 127 <= 124 for x <= 0."""
     rng = np.random.default_rng(4)
