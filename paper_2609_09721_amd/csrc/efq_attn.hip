@@ -53,8 +53,12 @@ constexpr float kLn6 = 1.79175946922805500081f;      // log 6, Eq. (z-def)
 constexpr int kWaveQ = 32;     // queries per wave (MFMA N)
 constexpr int kBc = 64;        // keys per tile (two 32-key microscaling blocks)
 
-// C16 fold table of EFQ-Softmax-LUT (Sec. II-D), nibble j = C16[j].
-constexpr unsigned long long kC16 = 0x7765543322111110ull;
+// C16 fold table of EFQ-Softmax-LUT (Sec. II-D) as bytes: byte j of the
+// 16-byte table (little-endian dwords kC16T0..3) is C16[j].
+constexpr unsigned kC16T0 = 0x01010100u;   // C16[0..3]   = 0 1 1 1
+constexpr unsigned kC16T1 = 0x02020101u;   // C16[4..7]   = 1 1 2 2
+constexpr unsigned kC16T2 = 0x05040303u;   // C16[8..11]  = 3 3 4 5
+constexpr unsigned kC16T3 = 0x07070605u;   // C16[12..15] = 5 6 7 7
 
 // ---------------------------------------------------------------- helpers
 __device__ __forceinline__ int cvt_flr(float x) {
@@ -138,6 +142,7 @@ struct PgenArgs {
   float scale;   // softmax scale
   float sh;      // fl(scale * h)
   float sh32;    // 32 fl(scale * h)   (EFQ code argument, exact)
+  float sh16;    // 16 fl(scale * h)   (LUT index argument, exact)
   float c;       // fl(log 6 + tau)
   float negh;    // -h
   float l2s;     // fl(scale * log2 e)   (exp-then-quantize)
@@ -150,9 +155,9 @@ struct PgenOut {
 };
 
 struct PgenState {
-  float bias[2];      // per window: LUT B = -(m + k_b log2 + log6 + tau) h,
-                      // EFQ fl(32 B + 31.5)
-  unsigned d[2];      // EFQ: byte-packed codes of the current dword
+  float bias[2];      // per window, with B = -(m + k_b log2 + log6 + tau) h:
+                      // EFQ fl(32 B + 31.5), LUT fl(16 B + 15.5)
+  unsigned d[2];      // EFQ, LUT: byte-packed codes / indices of the current dword
   float sc[2];        // EXPQ: 2^k_b per window (fp32 scale of the conversion)
   float mq;           // EXPQ: running maximum in log2 units
   int scale_b;        // E8M0 of the lane's own block
@@ -160,12 +165,6 @@ struct PgenState {
   unsigned w[4];      // packed codes: window 0 regs 0-7, 8-15, window 1 ...
 };
 
-template <int SH>
-__device__ __forceinline__ unsigned lshl_add_imm(int v, unsigned acc) {
-  unsigned r;
-  asm("v_lshl_add_u32 %0, %1, %2, %3" : "=v"(r) : "v"(v), "n"(SH), "v"(acc));
-  return r;
-}
 
 template <int KIND>
 __device__ __forceinline__ void pg_max(const f32x16& s0, const f32x16& s1, float& pm0, float& pm1) {
@@ -231,26 +230,43 @@ __device__ __forceinline__ void pg_params(float pm0, float pm1, float& m, const 
       // fma(acc, scale h, bias), bias = -(m + k_b log2 + log6 + tau) h
       const float off = (float)kb * kLn2 + pa.c;
       float b0 = (m + off) * pa.negh;
-      // EFQ: w_t = fma(acc_t, 32 scale h, fl(32 B + 31.5)) ~ 32 (u_t + 1) - 1/2
+      // EFQ: w_t = fma(acc_t, 32 scale h, fl(32 B + 31.5)) ~ 32 (u_t + 1) - 1/2;
+      // LUT: the same with 16 levels, fl(16 B + 15.5)
       if constexpr (KIND == EFQ_PGEN_EFQ) b0 = __builtin_fmaf(b0, 32.0f, 31.5f);
+      else b0 = __builtin_fmaf(b0, 16.0f, 15.5f);
       float b1 = b0;
       swap32f(b0, b1);                          // (bias of block 0, bias of block 1)
       st.bias[0] = b0;
       st.bias[1] = b1;
       st.scale_b = kb + 127;
-      // LUT: packed codes start at 0x11111111, each element adds (c - 1)
-      st.w[0] = st.w[1] = st.w[2] = st.w[3] = 0x11111111u;
     }
   }
 }
 
 // EFQ-Softmax-LUT, Sec. II-D: the 16-level index j16 = clip(floor(u) + 1,
-// 0, 15) of u = (z_t - tau16) h16, folded through C16; returns the code
-// minus one.
-__device__ __forceinline__ int pg_lut_code_m1(float acc, const PgenArgs& pa, float bias) {
-  const float u = __builtin_fmaf(acc, pa.sh, bias);
-  const int j = clampi(cvt_flr(u), -1, 14) + 1;
-  return (int)((kC16 >> (4 * j)) & 0xF) - 1;
+// 0, 15) of u = (z_t - tau16) h16 is bits 7..4 of sat[0,255](rne(w)),
+// w ~ 16 (u + 1) - 1/2 (the EFQ argument below with 16 levels), written to
+// byte BYTE of d; lut_fold then maps the four indices of d through C16.
+template <int BYTE>
+__device__ __forceinline__ unsigned pg_lut_byte(float acc, const PgenArgs& pa, float bias16,
+                                                unsigned d) {
+  const float w = __builtin_fmaf(acc, pa.sh16, bias16);
+  return __builtin_amdgcn_cvt_pk_u8_f32(w, BYTE, BYTE == 0 ? 0u : d);
+}
+
+// C16[j16] for the four LUT indices in bits 7..4 of the bytes of d: two
+// byte-permute lookups (entries 0..7 and 8..15, selected by the low three
+// index bits) and a per-byte select on index bit 3 (bit 7 of the byte,
+// spread over the byte by the sign-replicating selectors 8..11).
+__device__ __forceinline__ unsigned lut_fold(unsigned d) {
+  const unsigned sel = (d >> 4) & 0x07070707u;
+  const unsigned lo = __builtin_amdgcn_perm(kC16T1, kC16T0, sel);
+  const unsigned hi = __builtin_amdgcn_perm(kC16T3, kC16T2, sel);
+  // in[] = {d bytes 0..3, (d << 8) bytes 0..3}: selector 8 (9) replicates
+  // bit 7 of in[1] (in[3]) = d byte 1 (3); 10 (11) of in[5] (in[7]) = d byte
+  // 0 (2)
+  const unsigned mask = __builtin_amdgcn_perm(d << 8, d, 0x090B080Au);
+  return (hi & mask) | (lo & ~mask);
 }
 
 // EFQ code of one score into byte BYTE of d: c = clip(floor(u) + 1, 0, 7)
@@ -284,9 +300,12 @@ __device__ __forceinline__ void pg_pair(const f32x16& s0, const f32x16& s1, cons
         st.w[DW] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(st.w[DW], p2, p3, st.sc[WIN], J + 1);
       }
     } else if constexpr (KIND == EFQ_PGEN_LUT) {
-      st.w[DW] = lshl_add_imm<4 * elem_nibble(J)>(pg_lut_code_m1(s[R], pa, st.bias[WIN]), st.w[DW]);
-      st.w[DW] = lshl_add_imm<4 * elem_nibble(J + 1)>(pg_lut_code_m1(s[R + 1], pa, st.bias[WIN]),
-                                                      st.w[DW]);
+      // as EFQ below: elements 0..3 into the bytes of d[0], 4..7 of d[1];
+      // the folded codes (0..7, one per byte) merge into nibbles
+      unsigned& d = st.d[J >> 2];
+      d = pg_lut_byte<J & 3>(s[R], pa, st.bias[WIN], d);
+      d = pg_lut_byte<(J & 3) + 1>(s[R + 1], pa, st.bias[WIN], d);
+      if constexpr (J == 6) st.w[DW] = lut_fold(st.d[0]) | (lut_fold(st.d[1]) << 4);
     } else {
       // elements 0..3 of the dword into the bytes of d[0], 4..7 into d[1]
       unsigned& d = st.d[J >> 2];
@@ -1214,6 +1233,7 @@ attn_pp_kernel(const void* __restrict__ q, const void* __restrict__ k,
   w.pa.scale = a.scale;
   w.pa.sh = a.scale * a.h;
   w.pa.sh32 = 32.0f * w.pa.sh;
+  w.pa.sh16 = 16.0f * w.pa.sh;
   w.pa.c = kLn6 + a.tau;
   w.pa.negh = -a.h;
   w.pa.l2s = a.scale * kInvLn2;
@@ -1311,6 +1331,7 @@ __global__ __launch_bounds__(64) void pgen_kernel(const float* __restrict__ x,
   pa.scale = 1.0f;
   pa.sh = 1.0f * a.h;
   pa.sh32 = 32.0f * pa.sh;
+  pa.sh16 = 16.0f * pa.sh;
   pa.c = kLn6 + a.tau;
   pa.negh = -a.h;
   pa.l2s = 1.0f * kInvLn2;
@@ -1349,6 +1370,7 @@ __global__ __launch_bounds__(256) void pgen_bench_kernel(int iters, float tau, f
   pa.scale = 0.0883883461f;
   pa.sh = pa.scale * h;
   pa.sh32 = 32.0f * pa.sh;
+  pa.sh16 = 16.0f * pa.sh;
   pa.c = kLn6 + tau;
   pa.negh = -h;
   pa.l2s = pa.scale * kInvLn2;
