@@ -773,14 +773,20 @@ constexpr int kPPK = kPP + 1;              // K ring depth
 constexpr int kPPV = kPP + 2;              // V~ ring depth
 // Wave priorities (s_setprio) of the two phases, per probability stage: the
 // issue arbiter of a SIMD favours the wave whose work is on the critical
-// path.  EFQ: the VALU phase (max, parameters, rescale) is the longer one;
-// exp-then-quantize and LUT: the matrix phase carries their heavier code
+// path.  EFQ and LUT: the VALU phase (max, parameters, rescale) is the
+// longer one; exp-then-quantize: the matrix phase carries its heavier code
 // step.  Measured, not derived (both orders were timed).
 #ifndef EFQ_PRIO_EFQ_M
 #define EFQ_PRIO_EFQ_M 0
 #endif
 #ifndef EFQ_PRIO_EFQ_V
 #define EFQ_PRIO_EFQ_V 3
+#endif
+#ifndef EFQ_PRIO_LUT_M
+#define EFQ_PRIO_LUT_M 0
+#endif
+#ifndef EFQ_PRIO_LUT_V
+#define EFQ_PRIO_LUT_V 3
 #endif
 #ifndef EFQ_PRIO_OTHER_M
 #define EFQ_PRIO_OTHER_M 3
@@ -1033,8 +1039,10 @@ struct PPWave {
   // the pre-read needs registers the bf16 exp-then-quantize variants lack
   static constexpr bool kPreOn = kKPre && (Q8 || EFQ_KPRE_BF16);
   static constexpr int kMPrio = KIND == EFQ_PGEN_EFQ ? EFQ_PRIO_EFQ_M
+                                : KIND == EFQ_PGEN_LUT ? EFQ_PRIO_LUT_M
                                 : KIND == EFQ_PGEN_NOOP ? 0 : EFQ_PRIO_OTHER_M;
   static constexpr int kVPrio = KIND == EFQ_PGEN_EFQ ? EFQ_PRIO_EFQ_V
+                                : KIND == EFQ_PGEN_LUT ? EFQ_PRIO_LUT_V
                                 : KIND == EFQ_PGEN_NOOP ? 0 : EFQ_PRIO_OTHER_V;
 
   // Matrix phase M(j): with QK the scores of tile j into sn, and with CODES
