@@ -826,13 +826,17 @@ __device__ __forceinline__ f32x4 rowsum_mfma(const i32x8& sel, const i32x8& b8, 
 // (scores sc0, sc1, block parameters in st) runs on the VALU in the shadow
 // of those MFMAs, one slice per k-step region (sched_barrier keeps the
 // regions in order), then its P~V and P~1 MFMAs close the phase.
+#ifndef EFQ_QK_PD
+#define EFQ_QK_PD 3
+#endif
+constexpr int kQkPD = EFQ_QK_PD;   // bf16 K operand reads kept this many k-steps ahead
 template <int D, int KIND, bool QK, int I>
 __device__ __forceinline__ void mc_regions(const uint8_t* p0, const uint8_t* p1, bf16x8* a0,
                                            bf16x8* a1, const bf16x8* qreg, f32x16& sn0,
                                            f32x16& sn1, const f32x16& sc0, const f32x16& sc1,
                                            const PgenArgs& pa, PgenState& st) {
   constexpr int KK = D / 16;
-  constexpr int PD = KK < 3 ? KK : 3;
+  constexpr int PD = KK < kQkPD ? KK : kQkPD;
   if constexpr (I < KK) {
     if constexpr (QK) {
       sn0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[I], qreg[I], sn0, 0, 0, 0);
@@ -858,7 +862,7 @@ __device__ __forceinline__ PgenOut mma_phase(const uint8_t* kbuf, const bf16x8* 
                                              f32x16& sn1, const f32x16& sc0, const f32x16& sc1,
                                              const PgenArgs& pa, PgenState& st) {
   constexpr int KK = D / 16;
-  constexpr int PD = KK < 3 ? KK : 3;
+  constexpr int PD = KK < kQkPD ? KK : kQkPD;
   const uint8_t* p0 = kbuf + lane * 16;
   const uint8_t* p1 = p0 + KK * 1024;
   bf16x8 a0[KK], a1[KK];
@@ -1044,6 +1048,14 @@ struct PPWave {
   static constexpr int kVPrio = KIND == EFQ_PGEN_EFQ ? EFQ_PRIO_EFQ_V
                                 : KIND == EFQ_PGEN_LUT ? EFQ_PRIO_LUT_V
                                 : KIND == EFQ_PGEN_NOOP ? 0 : EFQ_PRIO_OTHER_V;
+  // The P~V and P~1 MFMAs have no memory effects, so the compiler may sink
+  // them past the phase barrier into the VALU phase, next to their first
+  // use.  On the FP8 Q K^T path the stages whose matrix phase is the
+  // heavier one (exp-then-quantize, the no-op stage) issue them in the
+  // matrix phase instead (an empty asm reads their results there); EFQ and
+  // LUT, and every stage on the bf16 path, keep the compiler's placement.
+  // Measured, both ways.
+  static constexpr bool kPvFence = Q8 && KIND != EFQ_PGEN_EFQ && KIND != EFQ_PGEN_LUT;
 
   // Matrix phase M(j): with QK the scores of tile j into sn, and with CODES
   // the codes of tile j-1 (scores sc) in the shadow of those MFMAs, then its
@@ -1073,6 +1085,13 @@ struct PPWave {
       const i32x8 b8 = i32x8{(int)po.bop[0], (int)po.bop[1], (int)po.bop[2], (int)po.bop[3], 0, 0, 0, 0};
       pv_slabs<NS>(oacc, vop, b8, po.scale_b);
       lacc = rowsum_mfma(sel, b8, lacc, po.scale_b);
+#if defined(__HIP_DEVICE_COMPILE__)
+      if constexpr (kPvFence) {
+#pragma unroll
+        for (int s = 0; s < NS; ++s) asm volatile("" ::"v"(oacc[s]));
+        asm volatile("" ::"v"(lacc));
+      }
+#endif
     }
   }
 
