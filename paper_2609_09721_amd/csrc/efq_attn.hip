@@ -711,14 +711,27 @@ struct VOps {
   int sv;
 };
 
+// Lane offsets of the V~ operand reads within a ring slot: codes, scales.
 template <int D>
-__device__ __forceinline__ void read_v(const uint8_t* vb, int lane, VOps<D>& v) {
+__device__ __forceinline__ int vop_offset(int lane) {
+  return ((lane >> 5) * D + (lane & 31)) * 16;
+}
+template <int D>
+__device__ __forceinline__ int vscale_offset(int lane) {
+  return Smem<D, 1, 1>::kVc + (lane >> 5) * D + (lane & 31) * (D / 32);
+}
+
+template <int D>
+__device__ __forceinline__ void read_v(const uint8_t* vb, int voff, int vsoff, VOps<D>& v) {
   constexpr int NS = D / 32;
-  const int half = lane >> 5;
-  const uint8_t* vc = vb + (half * D + (lane & 31)) * 16;
+  // one address per slot: the slab reads take immediate offsets from it
+  typedef __attribute__((address_space(3))) const uint8_t* lds_cptr;
+  lds_cptr vc = (lds_cptr)(vb + voff);
+  asm volatile("" : "+v"(vc));
 #pragma unroll
-  for (int s = 0; s < NS; ++s) v.a[s] = *(const u32x4*)(vc + s * 32 * 16);
-  const uint8_t* vsp = vb + Smem<D, 1, 1>::kVc + half * D + (lane & 31) * NS;
+  for (int s = 0; s < NS; ++s)
+    v.a[s] = *(__attribute__((address_space(3))) const u32x4*)(vc + s * 32 * 16);
+  const uint8_t* vsp = vb + vsoff;
   if constexpr (NS == 4) v.sv = *(const int*)vsp;
   else v.sv = *(const unsigned short*)vsp;
 }
@@ -1040,6 +1053,8 @@ struct PPWave {
   PgenArgs pa;
   PgenState st;           // block parameters of the tile between V(j) and M(j+1)
   int lane, half, my_q, vis_end;
+  int vis_min;            // wave-uniform minimum of vis_end
+  int voff, vsoff;        // lane offsets of the V~ operand reads
   // the pre-read needs registers the bf16 exp-then-quantize variants lack
   static constexpr bool kPreOn = kKPre && (Q8 || EFQ_KPRE_BF16);
   static constexpr int kMPrio = KIND == EFQ_PGEN_EFQ ? EFQ_PRIO_EFQ_M
@@ -1106,9 +1121,9 @@ struct PPWave {
                                          f32x16& s0, f32x16& s1, VOps<D>& vop, KPre<D, Q8>& kp) {
     if constexpr (kMPrio != kVPrio) __builtin_amdgcn_s_setprio(kVPrio);
     if constexpr (kPreOn) kp.read(kbuf0 + ((j + 1) % kPPK) * SmemPP<D, Q8>::kK, lane);
-    read_v<D>(vbuf0 + (j % kPPV) * SmemPP<D, Q8>::kV, lane, vop);
-    const int lim = vis_end - j * kBc;
-    if (__builtin_amdgcn_ballot_w64(lim < kBc) != 0ull) mask_tile(s0, s1, lim, half);
+    read_v<D>(vbuf0 + (j % kPPV) * SmemPP<D, Q8>::kV, voff, vsoff, vop);
+    // some lane's visible keys end inside this tile
+    if ((j + 1) * kBc > vis_min) mask_tile(s0, s1, vis_end - j * kBc, half);
     float pm0, pm1;
     pg_max<KIND>(s0, s1, pm0, pm1);
     pg_params<KIND>(pm0, pm1, m, pa, st);
@@ -1238,6 +1253,13 @@ attn_pp_kernel(const void* __restrict__ q, const void* __restrict__ k,
   const int ntiles = (kv_end + kBc - 1) / kBc;
   const int wtiles = (wave_end + kBc - 1) / kBc;
   w.vis_end = CAUSAL ? min(a.Sk, w.my_q + 1) : a.Sk;
+  // lane 0 holds the wave's first query, whose visible range is the shortest
+  w.vis_min = __builtin_amdgcn_readfirstlane(CAUSAL ? min(a.Sk, q_wave0 + 1) : a.Sk);
+  // the lane offsets stay in registers across the loop instead of being
+  // recomputed from the lane index in every phase
+  w.voff = vop_offset<D>(w.lane);
+  w.vsoff = vscale_offset<D>(w.lane);
+  asm volatile("" : "+v"(w.voff), "+v"(w.vsoff));
 
   std::conditional_t<Q8, KLoad8<D, kPPWaves>, KLoad<D, kPPWaves>> kload;
   int k_issued;
