@@ -1,0 +1,95 @@
+"""The LDS ring schedule of the ping-pong attention kernel, checked on the CPU.
+
+The kernel streams K and V~ tiles into LDS rings with direct-to-LDS loads and
+synchronises its eight waves with a workgroup barrier at the end of every odd
+phase only.  This test replays the schedule for every tile count up to 24,
+every per-wave tile count (causal waves see fewer tiles than their
+workgroup) and both wave groups, with and without the K pre-read, and checks
+the two properties the ring needs:
+
+* a tile is read only after the barrier that follows its landing wait;
+* a slot is refilled only after every read of its previous tile has been
+  consumed, in an earlier barrier interval.
+
+Barrier interval k holds phases 2k and 2k+1 (the barrier ends phase 2k+1);
+waves in the same interval are unordered.
+"""
+import os
+import re
+
+import pytest
+
+SRC = os.path.join(os.path.dirname(__file__), "..", "paper_2609_09721_amd", "csrc", "efq_attn.hip")
+
+P = 3            # tiles streamed ahead
+KEEP = P - 2     # batches left in flight at odd phases (the K pre-read is compiled in)
+KRING, VRING = P + 1, P + 2
+
+
+def test_constants_match_kernel_source():
+    src = open(SRC).read()
+    assert re.search(r"#define EFQ_KPRE 1\b", src)
+    assert re.search(r"#define EFQ_PREFETCH \(2 \+ EFQ_KPRE\)", src)
+    assert "constexpr int kPPK = kPP + 1;" in src
+    assert "constexpr int kPPV = kPP + 2;" in src
+    assert "constexpr int kKeep = kPP - 1 - (kKPre ? 1 : 0);" in src
+    # the barrier sits in the odd-phase branch of the phase end
+    end = src[src.index("auto end = [&]() {"):]
+    end = end[:end.index("};")]
+    odd = end[end.index("if (t & 1) {"):end.index("} else {")]
+    assert "wg_barrier();" in odd
+    assert "wg_barrier" not in end[end.index("} else {"):]
+
+
+def landing_phase(x):
+    """Odd phase at whose end every wave's load of tile x has completed."""
+    if x < 2:
+        return -1                       # resident before phase 0
+    # the fifo at odd phase 2k+1 holds tiles k+2 .. k+P; all but the last
+    # KEEP have landed, so tile x lands at k = x - P + KEEP
+    return 2 * (x - P + KEEP) + 1
+
+
+def interval(phase):
+    return phase // 2
+
+
+def wave_reads(T, G, pre):
+    """(slot kind, tile, read phase, consume phase) for one wave with T tiles."""
+    reads = []
+    for j in range(T):
+        m = 2 * j + G                   # M(j)
+        v = 2 * j + 1 + G               # V(j)
+        reads.append(("K", j, m, m))
+        reads.append(("V", j, v, v + 1))          # consumed by M(j+1) or F
+        if pre and j + 1 < T:
+            reads.append(("K", j + 1, v, v + 1))  # first operands of M(j+1)
+    return reads
+
+
+@pytest.mark.parametrize("pre", [False, True])
+def test_ring_schedule_is_safe(pre):
+    cases = 0
+    for ntiles in range(1, 25):
+        reads = []
+        for T in range(1, ntiles + 1):
+            for G in (0, 1):
+                reads += wave_reads(T, G, pre)
+        # every read happens after its tile's landing barrier
+        for kind, x, t, c in reads:
+            assert x < ntiles
+            assert interval(landing_phase(x)) < interval(t) or landing_phase(x) < 0, (kind, x, t)
+            cases += 1
+        # every refill comes after the consumption of the slot's previous tile
+        for x in range(P + 1, ntiles):
+            issue = 2 * (x - P)
+            for kind, ring in (("K", KRING), ("V", VRING)):
+                old = x - ring
+                if old < 0:
+                    continue
+                last = max((c for k, y, t, c in reads if k == kind and y == old), default=-1)
+                assert interval(last) < interval(issue), (kind, x, old, last, issue)
+        # every wave runs 2 ntiles + 2 phases, so all pass the same barriers
+        phases = 2 * ntiles + 2
+        assert sum(1 for t in range(phases) if t & 1) == ntiles + 1
+    assert cases > 1000
