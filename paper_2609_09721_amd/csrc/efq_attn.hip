@@ -764,9 +764,9 @@ __device__ __forceinline__ void mask_tile(f32x16& s0, f32x16& s1, int lim, int h
 // Eight waves per workgroup (two per SIMD, 256 queries) in two groups of
 // four.  Each tile is split into a matrix-core phase M(j) = P~V of tile j-1
 // and S(j) = K(j) Q^T, and a VALU phase V(j) = the probability stage of
-// tile j and the history rescale.  The groups run opposite phases between
-// workgroup barriers, so on every SIMD one wave feeds the matrix core while
-// the other runs the probability stage:
+// tile j and the history rescale.  The groups run opposite phases, so on
+// every SIMD one wave feeds the matrix core while the other runs the
+// probability stage (a workgroup barrier every four phases re-aligns them):
 //   phase 2j:    group 0 runs M(j),  group 1 runs V(j-1)
 //   phase 2j+1:  group 0 runs V(j),  group 1 runs M(j)
 // K(j) is read in phases 2j-1 .. 2j+1 (the first operands of a matrix phase
@@ -779,11 +779,12 @@ constexpr int kPPThreads = 64 * kPPWaves;
 #define EFQ_KPRE 1                         // read K operands one phase early
 #endif
 #ifndef EFQ_PREFETCH
-#define EFQ_PREFETCH (2 + EFQ_KPRE)
+#define EFQ_PREFETCH (3 + EFQ_KPRE)
 #endif
-constexpr int kPP = EFQ_PREFETCH;          // tiles streamed ahead (>= 2)
-constexpr int kPPK = kPP + 1;              // K ring depth
-constexpr int kPPV = kPP + 2;              // V~ ring depth
+constexpr int kPP = EFQ_PREFETCH;          // tiles streamed ahead (>= 3)
+constexpr int kPPK = kPP + 2;              // K ring depth
+constexpr int kPPV = kPP + 3;              // V~ ring depth
+constexpr int kBarPhases = 4;              // phases between workgroup barriers
 // Wave priorities (s_setprio) of the two phases, per probability stage: the
 // issue arbiter of a SIMD favours the wave whose work is on the critical
 // path.  EFQ and LUT: the VALU phase (max, parameters, rescale) is the
@@ -811,7 +812,7 @@ constexpr int kPPV = kPP + 2;              // V~ ring depth
 #define EFQ_KPRE_BF16 0                    // also on the bf16 Q K^T path
 #endif
 constexpr bool kKPre = EFQ_KPRE != 0;
-constexpr int kKeep = kPP - 1 - (kKPre ? 1 : 0);   // batches left in flight at odd phases
+constexpr int kKeep = kPP - 2 - (kKPre ? 1 : 0);   // batches left in flight at odd phases
 static_assert(kKeep >= 0, "prefetch distance too short for the K pre-read");
 template <int D, bool Q8 = false>
 using SmemPP = Smem<D, kPPK, kPPV, Q8>;
@@ -1143,17 +1144,17 @@ struct PPWave {
 // and V~(j) in phases 2j+1, 2j+2.  Even phases t = 2j >= 2 start by
 // streaming tile j+P (K and V~); odd phases end by waiting until only the
 // loads of the last E even phases are outstanding (loads complete in
-// order), E = P-2 with the pre-read, else P-1, and then by a workgroup
-// barrier.  A load issued in phase 2j has therefore landed by the end of
-// phase 2(j+P-E)-1: with the pre-read (P = 3, E = 1) that is 2(j+P)-3, and
-// the barrier after it precedes the pre-read of K(j+P) in phase 2(j+P)-1.
-// The slots it overwrites (K(j-1) in a ring of P+1, V~(j-2) in a ring of
-// P+2) were last read, and the reads consumed, by phase 2j-1, before the
-// barrier that ends it.  Every ordering the rings need is thus between an
-// odd phase and a later one; a barrier after an even phase would only hold
-// the two groups in lock step (dropping it measured 2-6 % faster).  Every
-// wave runs 2 ntiles + 2 phases and passes ntiles + 1 barriers.  Scores
-// alternate between two register sets.
+// order), E = P-3 with the pre-read, else P-2; phases 4k+3 then end with a
+// workgroup barrier (waves between two barriers are unordered).  A load
+// issued in phase 2j has landed by the end of phase 2(j+P-E)-1, with the
+// pre-read (P = 4, E = 1) 2(j+P)-5, and the next barrier, at the end of
+// phase 2(j+P)-5 or 2(j+P)-3, precedes the pre-read of K(j+P) in phase
+// 2(j+P)-1.  The slots it overwrites (K(j-2) in a ring of P+2, V~(j-3) in a
+// ring of P+3) were last read, and the reads consumed, by phase 2j-3,
+// before a barrier that precedes phase 2j.  Fewer barriers let the groups
+// drift within four phases; each one dropped measured 1-6 % faster than a
+// barrier per phase.  Every wave runs 2 ntiles + 2 phases, so all pass the
+// same barriers.  Scores alternate between two register sets.
 template <int G, int D, int KIND, bool DUMP, bool Q8, typename Stream>
 __device__ __forceinline__ void pp_schedule(PPWave<D, KIND, DUMP, Q8>& w, int T, int ntiles,
                                             const uint8_t* kbuf0, const uint8_t* vbuf0,
@@ -1179,7 +1180,8 @@ __device__ __forceinline__ void pp_schedule(PPWave<D, KIND, DUMP, Q8>& w, int T,
 #pragma unroll
       for (int i = kPP - 1 - kKeep; i < kPP - 1; ++i) n += fifo[i];
       wait_vmem_le(n);
-      wg_barrier();
+      if ((t & (kBarPhases - 1)) == kBarPhases - 1) wg_barrier();
+      else __builtin_amdgcn_sched_barrier(0);
     } else {
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -1298,7 +1300,7 @@ attn_pp_kernel(const void* __restrict__ q, const void* __restrict__ k,
   w.sel = rowsum_selector(w.lane);
   w.m = -INFINITY;
 
-  // Streams tile x (K into ring slot x % (P+1), V~ into x % (P+2)) if it
+  // Streams tile x (K into ring slot x % (P+2), V~ into x % (P+3)) if it
   // exists; returns the number of loads issued.
   auto load_tile = [&](int x) {
     if (x >= ntiles) return 0;

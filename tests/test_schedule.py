@@ -1,8 +1,8 @@
 """The LDS ring schedule of the ping-pong attention kernel, checked on the CPU.
 
 The kernel streams K and V~ tiles into LDS rings with direct-to-LDS loads and
-synchronises its eight waves with a workgroup barrier at the end of every odd
-phase only.  This test replays the schedule for every tile count up to 24,
+synchronises its eight waves with a workgroup barrier at the end of every
+fourth phase only.  This test replays the schedule for every tile count up to 24,
 every per-wave tile count (causal waves see fewer tiles than their
 workgroup) and both wave groups, with and without the K pre-read, and checks
 the two properties the ring needs:
@@ -11,7 +11,7 @@ the two properties the ring needs:
 * a slot is refilled only after every read of its previous tile has been
   consumed, in an earlier barrier interval.
 
-Barrier interval k holds phases 2k and 2k+1 (the barrier ends phase 2k+1);
+Barrier interval k holds phases 4k .. 4k+3 (the barrier ends phase 4k+3);
 waves in the same interval are unordered.
 """
 import os
@@ -21,24 +21,27 @@ import pytest
 
 SRC = os.path.join(os.path.dirname(__file__), "..", "paper_2609_09721_amd", "csrc", "efq_attn.hip")
 
-P = 3            # tiles streamed ahead
-KEEP = P - 2     # batches left in flight at odd phases (the K pre-read is compiled in)
-KRING, VRING = P + 1, P + 2
+P = 4            # tiles streamed ahead
+KEEP = P - 3     # batches left in flight at odd phases (the K pre-read is compiled in)
+KRING, VRING = P + 2, P + 3
+BAR = 4          # phases per barrier interval
 
 
 def test_constants_match_kernel_source():
     src = open(SRC).read()
     assert re.search(r"#define EFQ_KPRE 1\b", src)
-    assert re.search(r"#define EFQ_PREFETCH \(2 \+ EFQ_KPRE\)", src)
-    assert "constexpr int kPPK = kPP + 1;" in src
-    assert "constexpr int kPPV = kPP + 2;" in src
-    assert "constexpr int kKeep = kPP - 1 - (kKPre ? 1 : 0);" in src
-    # the barrier sits in the odd-phase branch of the phase end
+    assert re.search(r"#define EFQ_PREFETCH \(3 \+ EFQ_KPRE\)", src)
+    assert "constexpr int kPPK = kPP + 2;" in src
+    assert "constexpr int kPPV = kPP + 3;" in src
+    assert "constexpr int kBarPhases = 4;" in src
+    assert "constexpr int kKeep = kPP - 2 - (kKPre ? 1 : 0);" in src
+    # the barrier sits in the odd-phase branch of the phase end, once every
+    # kBarPhases phases
     end = src[src.index("auto end = [&]() {"):]
     end = end[:end.index("};")]
-    odd = end[end.index("if (t & 1) {"):end.index("} else {")]
-    assert "wg_barrier();" in odd
-    assert "wg_barrier" not in end[end.index("} else {"):]
+    odd = end[end.index("if (t & 1) {"):end.index("} else {\n      __builtin_amdgcn_sched_barrier(0);\n    }\n    ++t;")]
+    assert "if ((t & (kBarPhases - 1)) == kBarPhases - 1) wg_barrier();" in odd
+    assert end.count("wg_barrier") == 1
 
 
 def landing_phase(x):
@@ -51,7 +54,7 @@ def landing_phase(x):
 
 
 def interval(phase):
-    return phase // 2
+    return phase // BAR
 
 
 def wave_reads(T, G, pre):
@@ -91,5 +94,5 @@ def test_ring_schedule_is_safe(pre):
                 assert interval(last) < interval(issue), (kind, x, old, last, issue)
         # every wave runs 2 ntiles + 2 phases, so all pass the same barriers
         phases = 2 * ntiles + 2
-        assert sum(1 for t in range(phases) if t & 1) == ntiles + 1
+        assert sum(1 for t in range(phases) if t % BAR == BAR - 1) == phases // BAR
     assert cases > 1000
