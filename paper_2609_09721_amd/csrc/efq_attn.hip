@@ -1159,26 +1159,23 @@ template <int G, int D, int KIND, bool DUMP, bool Q8, typename Stream>
 __device__ __forceinline__ void pp_schedule(PPWave<D, KIND, DUMP, Q8>& w, int T, int ntiles,
                                             const uint8_t* kbuf0, const uint8_t* vbuf0,
                                             const AttnArgs& a, int b, int hq,
-                                            const int (&fifo0)[kPP - 1], Stream stream) {
+                                            int per_tile, Stream stream) {
   f32x16 sa0, sa1, sb0, sb1;
   VOps<D> vop;
   KPre<D, Q8> kp;      // first K operands of the next matrix phase
-  int fifo[kPP - 1];   // loads issued by the last P-1 even phases, oldest first
-#pragma unroll
-  for (int i = 0; i < kPP - 1; ++i) fifo[i] = fifo0[i];
   int t = 0;   // phase
   auto begin = [&]() {
-    if ((t & 1) == 0 && t >= 2) {
-#pragma unroll
-      for (int i = 0; i + 1 < kPP - 1; ++i) fifo[i] = fifo[i + 1];
-      fifo[kPP - 2] = stream(t >> 1);
-    }
+    if ((t & 1) == 0 && t >= 2) stream(t >> 1);
   };
   auto end = [&]() {
     if (t & 1) {
+      // the batches of the last kKeep even phases 2(k-i) (tiles k-i+P; the
+      // prologue stands in for phases <= 0) may stay in flight: per_tile
+      // loads each, none for a tile past the end
+      const int k = t >> 1;
       int n = 0;
 #pragma unroll
-      for (int i = kPP - 1 - kKeep; i < kPP - 1; ++i) n += fifo[i];
+      for (int i = 0; i < kKeep; ++i) n += k - i + kPP < ntiles ? per_tile : 0;
       wait_vmem_le(n);
       if ((t & (kBarPhases - 1)) == kBarPhases - 1) wg_barrier();
       else __builtin_amdgcn_sched_barrier(0);
@@ -1311,15 +1308,11 @@ attn_pp_kernel(const void* __restrict__ q, const void* __restrict__ k,
   };
   // prologue: tiles 0 .. P; tiles 0 and 1 resident, 2 .. P in flight (the
   // loads of the last P-1 even phases before phase 2)
-  int fifo[kPP - 1];
   load_tile(0);
   load_tile(1);
   int pending = 0;
 #pragma unroll
-  for (int x = 2; x <= kPP; ++x) {
-    fifo[x - 2] = load_tile(x);
-    pending += fifo[x - 2];
-  }
+  for (int x = 2; x <= kPP; ++x) pending += load_tile(x);
   wait_vmem_le(pending);
   __syncthreads();
 
@@ -1327,9 +1320,9 @@ attn_pp_kernel(const void* __restrict__ q, const void* __restrict__ k,
   auto stream = [&](int j) { return load_tile(j + kPP); };
 
   if (group == 0)
-    pp_schedule<0>(w, wtiles, ntiles, kbuf0, vbuf0, a, b, hq, fifo, stream);
+    pp_schedule<0>(w, wtiles, ntiles, kbuf0, vbuf0, a, b, hq, k_issued + v_issued, stream);
   else
-    pp_schedule<1>(w, wtiles, ntiles, kbuf0, vbuf0, a, b, hq, fifo, stream);
+    pp_schedule<1>(w, wtiles, ntiles, kbuf0, vbuf0, a, b, hq, k_issued + v_issued, stream);
   wait_vmem();   // no load may still target LDS when the wave leaves
 
   // O = A / l as A * (1 / l): one division per row instead of one per
