@@ -141,16 +141,20 @@ def counters(d: str, out: str, command: str):
         fh.write("# cycles per XCD = GRBM_GUI_ACTIVE / 8; MFMA busy and VALU active are per SIMD "
                  "(SQ_ACTIVE_INST_VALU is in quad-cycles, summed over the SIMD's waves)\n")
         fh.write("# VALU per score: wave instructions x 64 lanes / visible (query, key) pairs\n")
+        fh.write("# co-exec: cycles in which the matrix core was busy and a VALU instruction "
+                 "issued (SQ_VALU_MFMA_COEXEC_CYCLES), per SIMD\n")
         fh.write("# kernel | cycles | MFMA busy / cycles | VALU active / cycles | "
-                 "(MFMA + VALU) / cycles | VALU instr per SIMD | MFMA instr per SIMD | "
-                 "VALU per score | LDS instr per SIMD | bank-conflict cycles per LDS instr\n")
+                 "(MFMA + VALU) / cycles | co-exec / cycles | VALU instr per SIMD | "
+                 "MFMA instr per SIMD | VALU per score | LDS instr per SIMD | "
+                 "bank-conflict cycles per LDS instr\n")
         for key in sorted(acc):
             c = acc[key]
             cyc = c["GRBM_GUI_ACTIVE"] / xcds
             mf = c["SQ_VALU_MFMA_BUSY_CYCLES"] / simds
             va = 4 * c["SQ_ACTIVE_INST_VALU"] / simds
+            co = c.get("SQ_VALU_MFMA_COEXEC_CYCLES", float("nan")) / simds
             fh.write(f"{names[key]} | {cyc:.0f} | {mf / cyc:.3f} | {va / cyc:.3f} | "
-                     f"{(mf + va) / cyc:.3f} | {c['SQ_INSTS_VALU'] / simds:.0f} | "
+                     f"{(mf + va) / cyc:.3f} | {co / cyc:.3f} | {c['SQ_INSTS_VALU'] / simds:.0f} | "
                      f"{c['SQ_INSTS_MFMA'] / simds:.0f} | {c['SQ_INSTS_VALU'] * 64 / pairs:.2f} | "
                      f"{c.get('SQ_INSTS_LDS', 0) / simds:.0f} | "
                      f"{c.get('SQ_LDS_BANK_CONFLICT', 0) / max(c.get('SQ_INSTS_LDS', 0), 1):.4f}\n")
