@@ -13,6 +13,10 @@
 //                      matrix-core and VALU phases.
 //   pgen_kernel        the probability stage alone on given shifted scores.
 //   pgen_bench_kernel  register-resident throughput probe of that stage.
+//   rho_partial_kernel, rho_final_kernel
+//                      the relative Frobenius error of Alg. 3's calibration
+//                      objective, in fp64 with a fixed reduction order.
+//   fill_zero_kernel   zero fill of the dump buffers (blocks never reached).
 //
 // Register layout (v_mfma_f32_32x32x16_bf16, verified on gfx950): lane L of a
 // 64-lane wave holds column L%32 of the 32x32 result and rows
