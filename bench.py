@@ -98,8 +98,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
-              "(the kernel shards by (batch, head) with no communication; see the design notes)",
+        print("bench.py runs on exactly one GPU: the library has no multi-GPU path "
+              "(the kernel would shard by (batch, head) with no communication)",
               file=sys.stderr)
         sys.exit(2)
 
