@@ -75,13 +75,24 @@ CASES = [
     (1, 333, 333, 1, 1, 128, True),
 ]
 
+# Degenerate and boundary shapes (one key, one query, one tile and one key
+# past it, one query past a workgroup, grouped-query ratio 8, seq_k < 32).
+EDGE = [
+    (1, 1, 1, 1, 1, 64, True),
+    (1, 1, 1, 2, 1, 128, False),
+    (1, 65, 65, 1, 1, 128, True),
+    (1, 257, 257, 1, 1, 64, True),
+    (1, 7, 40, 8, 1, 64, False),
+    (3, 40, 5, 2, 1, 128, False),
+]
+
 
 def _unpack(codes_u8):
     c = codes_u8.astype(np.uint8)
     return np.stack([c & 0xF, c >> 4], axis=-1).reshape(*c.shape[:-1], -1)
 
 
-@pytest.mark.parametrize("case", CASES)
+@pytest.mark.parametrize("case", CASES + EDGE)
 @pytest.mark.parametrize("kind", ["efq", "lut"])
 def test_qk8_dump_exact_scores(B, orc, case, kind):
     """Dyadic Q and K (multiples of 1/2 up to 2) are exact in MXFP8 and every

@@ -147,8 +147,22 @@ CASES = [
     (1, 333, 333, 1, 1, 128, True),
 ]
 
+# Degenerate and boundary shapes: one key, one query, a partial first MX
+# block, exactly one tile and one key past it, one query past a 256-query
+# workgroup, grouped-query ratio 8 with seq_q < seq_k, seq_k < 32.
+EDGE = [
+    (1, 1, 1, 1, 1, 64, True),
+    (1, 1, 1, 2, 1, 128, False),
+    (1, 33, 33, 2, 2, 64, True),
+    (1, 64, 64, 1, 1, 128, True),
+    (1, 65, 65, 1, 1, 128, True),
+    (1, 257, 257, 1, 1, 64, True),
+    (1, 7, 40, 8, 1, 64, False),
+    (3, 40, 5, 2, 1, 128, False),
+]
 
-@pytest.mark.parametrize("case", CASES)
+
+@pytest.mark.parametrize("case", CASES + EDGE)
 @pytest.mark.parametrize("kind", ["efq", "lut"])
 def test_attn_dump_exact_scores(B, orc, case, kind):
     """Exact-score inputs: every Q.K partial sum is exact, so the fused
@@ -189,6 +203,28 @@ def test_attn_expq_exact_scores(B, orc, case, kind):
     assert np.mean(cg == co) > 1 - 1e-4
     og = out.cpu().numpy().transpose(0, 2, 1, 3).reshape(-1, D)
     assert np.max(np.abs(og - oo)) <= TOL
+
+
+def test_single_key_returns_its_value(B):
+    """Causal row 0 sees one key: p~ is the top code of the row maximum's
+    block and O_0 is that key's quantised value row."""
+    g = torch.Generator().manual_seed(5)
+    for D in (64, 128):
+        q = torch.randn(1, 1, 2, D, generator=g).to(torch.bfloat16)
+        k = torch.randn(1, 1, 1, D, generator=g).to(torch.bfloat16)
+        v = torch.randn(1, 1, 1, D, generator=g).to(torch.bfloat16)
+        for kind in ("efq", "lut", "expq", "expq6"):
+            out = B.attn_fwd(q.cuda(), k.cuda(), v.cuda(), D ** -0.5, True, kind)
+            vh = B.quant_v(v.cuda(), seq_q=1, heads_q=2)
+            cg, eg = B.vhat_natural(vh, B.Shape(1, 1, 1, 2, 1, D))
+            # dequantise key 0 of every column: E2M1 magnitude times 2^(E8M0 - 127)
+            mag = torch.tensor([0, 0.5, 1, 1.5, 2, 3, 4, 6], dtype=torch.float64)
+            c = cg[0, 0, 0, :].cpu().long()
+            sign = torch.where((c & 8) > 0, -1.0, 1.0).double()
+            ref = (mag[c & 7] * sign * torch.exp2(eg[0, 0, 0, :].cpu().double() - 127)).float()
+            for h in range(2):
+                err = (out[0, 0, h].cpu() - ref).abs().max().item()
+                assert err <= 1e-6 * max(1.0, ref.abs().max().item()), (D, kind, h, err)
 
 
 def test_tiny_config_all_rows(B, orc):
