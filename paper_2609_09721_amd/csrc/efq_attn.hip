@@ -820,6 +820,9 @@ constexpr int kKeep = kPP - 2 - (kKPre ? 1 : 0);   // batches left in flight at 
 static_assert(kKeep >= 0, "prefetch distance too short for the K pre-read");
 template <int D, bool Q8 = false>
 using SmemPP = Smem<D, kPPK, kPPV, Q8>;
+// one workgroup per CU: the rings must fit the 160 KB of LDS
+static_assert(SmemPP<128>::kTotal <= 160 * 1024 && SmemPP<128, true>::kTotal <= 160 * 1024,
+              "K and V~ rings exceed the LDS of a CU");
 
 // P~1 on the 16x16x128 FP4 MFMA.  Its B operand is the P~^T operand of the
 // P~V product as it sits in the lanes (lane l: query l % 32, key block
