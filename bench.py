@@ -43,22 +43,25 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_hash() -> str:
+def kernel_hash(src_path: str = None) -> str:
     """Hash of the kernel source's code: comments and blank lines are left
     out, so an edit of the comments keeps a counter summary valid."""
     import re
-    with open(os.path.join(ROOT, "paper_2609_09721_amd", "csrc", "efq_attn.hip")) as f:
+    if src_path is None:
+        src_path = os.path.join(ROOT, "paper_2609_09721_amd", "csrc", "efq_attn.hip")
+    with open(src_path) as f:
         src = f.read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    lines = [re.sub(r"//.*$", "", ln).rstrip() for ln in src.splitlines()]
+    lines = [re.sub(r"//.*$", "", ln).strip() for ln in src.splitlines()]
     code = "\n".join(ln for ln in lines if ln.strip())
     return hashlib.sha256(code.encode()).hexdigest()[:16]
 
 
-def read_traffic(workload: str):
+def read_traffic(workload: str, profiles_dir: str = None):
     """HBM bytes per launch of the attention kernel from the committed
     rocprofv3 counter summary, if it was taken on the current kernel source."""
-    path = os.path.join(ROOT, "profiles", f"attn_fwd_{workload}_traffic.txt")
+    path = os.path.join(profiles_dir or os.path.join(ROOT, "profiles"),
+                        f"attn_fwd_{workload}_traffic.txt")
     if not os.path.exists(path):
         return None
     kv = {}

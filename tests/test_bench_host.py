@@ -1,0 +1,46 @@
+"""Host-side logic of bench.py: the kernel-source hash that ties a committed
+HBM-traffic summary to the code it was measured on (no GPU needed)."""
+import os
+import shutil
+
+import bench
+
+SRC = os.path.join(os.path.dirname(bench.__file__), "paper_2609_09721_amd", "csrc", "efq_attn.hip")
+
+
+def _copy(tmp_path, edit=None):
+    text = open(SRC).read()
+    if edit:
+        text = edit(text)
+    p = tmp_path / "k.hip"
+    p.write_text(text)
+    return str(p)
+
+
+def test_hash_ignores_comments_and_blank_lines(tmp_path):
+    h = bench.kernel_hash(_copy(tmp_path))
+    assert h == bench.kernel_hash()
+    assert bench.kernel_hash(_copy(tmp_path, lambda t: "// a new note\n\n" + t)) == h
+    def block(t):
+        assert "constexpr int kBarPhases = 4;" in t
+        return t.replace("constexpr int kBarPhases = 4;",
+                         "/* a block\n   comment */ constexpr int kBarPhases = 4;  // note", 1)
+    assert bench.kernel_hash(_copy(tmp_path, block)) == h
+
+
+def test_hash_changes_with_code(tmp_path):
+    h = bench.kernel_hash()
+    edited = _copy(tmp_path, lambda t: t.replace("constexpr int kBarPhases = 4;",
+                                                 "constexpr int kBarPhases = 2;", 1))
+    assert bench.kernel_hash(edited) != h
+
+
+def test_traffic_only_for_matching_source(tmp_path):
+    d = tmp_path / "profiles"
+    d.mkdir()
+    f = d / "attn_fwd_w_traffic.txt"
+    f.write_text(f"# summary\ntraffic_bytes_per_launch = 123456\nkernel_hash = {bench.kernel_hash()}\n")
+    assert bench.read_traffic("w", str(d)) == 123456.0
+    f.write_text("traffic_bytes_per_launch = 123456\nkernel_hash = 0000000000000000\n")
+    assert bench.read_traffic("w", str(d)) is None
+    assert bench.read_traffic("missing", str(d)) is None
