@@ -3,8 +3,8 @@
 Plain, slow implementations of what the GPU path computes, written from the
 paper (Alg. 1 inside Alg. 2, Secs. II-III).  The C file ``efq_oracle.c``
 holds the attention recurrence, P-gen and V quantiser; ``twin.py`` holds an
-independent numpy rendering of the P-gen and V-quant rules used to
-cross-check it.  Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU
+independent numpy rendering of the P-gen and V-quant rules and of the
+Alg. 2 recurrence used to cross-check it.  Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU
 baseline of ``bench.py`` may import this package.  Nothing here imports the
 HIP package, and the HIP package never imports this.
 
@@ -36,15 +36,22 @@ C8 = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])  # Sec. II-B
 C16 = np.array([0, 1, 1, 1, 1, 1, 2, 2, 3, 3, 4, 5, 5, 6, 7, 7])  # Sec. II-D
 
 
+GCC_FLAGS = ["-O2", "-std=gnu99", "-Wall", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
+             "-shared", "-fPIC"]
+
+
+def compile_c(src: str, out: str, extra=()) -> str:
+    """gcc build of an oracle source file (no fast-math, no FMA contraction)."""
+    tmp = out + f".tmp{os.getpid()}"
+    subprocess.run(["gcc"] + GCC_FLAGS + list(extra) + [src, "-o", tmp, "-lm"], check=True)
+    os.replace(tmp, out)
+    return out
+
+
 def build(force: bool = True) -> str:
     """Compile the oracle with gcc (no fast-math, no FMA contraction)."""
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-        tmp = _LIB + f".tmp{os.getpid()}"
-        subprocess.run(
-            ["gcc", "-O2", "-std=gnu99", "-Wall", "-ffp-contract=off", "-fno-fast-math",
-             "-fopenmp", "-shared", "-fPIC", _SRC, "-o", tmp, "-lm"],
-            check=True)
-        os.replace(tmp, _LIB)
+        compile_c(_SRC, _LIB)
     return _LIB
 
 
@@ -56,21 +63,26 @@ def lib():
     if _lib is None:
         if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
             build(force=True)
-        L = ctypes.CDLL(_LIB)
-        P = ctypes.c_void_p
-        L.orc_pgen.argtypes = [P, ctypes.c_long, ctypes.c_int, ctypes.c_int, ctypes.c_float,
-                               ctypes.c_float, P, P]
-        L.orc_pgen_real.argtypes = [P, ctypes.c_long, ctypes.c_int, ctypes.c_int,
-                                    ctypes.c_double, ctypes.c_double, P, P, P]
-        L.orc_quant_v.argtypes = [P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, P, P]
-        L.orc_attn.argtypes = [P, P, P] + [ctypes.c_int] * 6 + [
-            ctypes.c_float, ctypes.c_int, ctypes.c_int, ctypes.c_float, ctypes.c_float,
-            ctypes.c_int, P, ctypes.c_long, P, P, P, P, P, P, ctypes.c_int, ctypes.c_int]
-        L.orc_quant_mxfp8.argtypes = [P, ctypes.c_long, ctypes.c_int, P, P]
-        for f in (L.orc_pgen, L.orc_pgen_real, L.orc_quant_v, L.orc_attn, L.orc_quant_mxfp8):
-            f.restype = ctypes.c_int
-        _lib = L
+        _lib = load(_LIB)
     return _lib
+
+
+def load(path: str):
+    """ctypes handle of an oracle build with the argument types set."""
+    L = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    L.orc_pgen.argtypes = [P, ctypes.c_long, ctypes.c_int, ctypes.c_int, ctypes.c_float,
+                           ctypes.c_float, P, P]
+    L.orc_pgen_real.argtypes = [P, ctypes.c_long, ctypes.c_int, ctypes.c_int,
+                                ctypes.c_double, ctypes.c_double, P, P, P]
+    L.orc_quant_v.argtypes = [P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, P, P]
+    L.orc_attn.argtypes = [P, P, P] + [ctypes.c_int] * 6 + [
+        ctypes.c_float, ctypes.c_int, ctypes.c_int, ctypes.c_float, ctypes.c_float,
+        ctypes.c_int, P, ctypes.c_long, P, P, P, P, P, P, ctypes.c_int, ctypes.c_int]
+    L.orc_quant_mxfp8.argtypes = [P, ctypes.c_long, ctypes.c_int, P, P]
+    for f in (L.orc_pgen, L.orc_pgen_real, L.orc_quant_v, L.orc_attn, L.orc_quant_mxfp8):
+        f.restype = ctypes.c_int
+    return L
 
 
 def _ptr(a: Optional[np.ndarray]):

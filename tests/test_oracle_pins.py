@@ -246,20 +246,68 @@ def test_vs_bruteforce_exp_then_quantize(orc, point, lo, hi):
     assert np.max(np.abs(s * orc.C8[codes] - p) / s) <= 3.0
 
 
-def test_contract_vs_real_valued(orc):
-    """The fp32 contract reproduces the fp64 step-by-step evaluation of
-    Alg. 1 except where (z - tau) h lies within 1e-4 of an integer."""
+U32 = 2.0 ** -24            # unit roundoff of fp32
+
+
+def _contract_vs_real(orc, x, mode, tau, h):
+    """Compare the fp32 decision contract with the fp64 step-by-step reading
+    of Alg. 1 (M_b, k_b = floor((M_b + log(2/9)) / log 2), z = x - k_b log 2 -
+    log 6, c = clip(floor((z - tau) h) + 1, 0, 7), or the 16-level LUT index).
+    Returns the per-code disagreement mask, the distances of the real u to
+    the nearest integer there, their stated bounds, and the same for k."""
+    lut = mode == orc.LUT_MODE
+    c32, e32 = orc.pgen(x, mode, tau, h)
+    c64, k64, u64 = orc.pgen_real(x.astype(np.float64), lut, tau, h)
+    rows, cols = x.shape
+    nb = k64.shape[1]
+    xp = np.concatenate([x, np.full((rows, nb * 32 - cols), -np.inf, np.float32)], 1)
+    Mb = xp.reshape(rows, nb, 32).max(axis=2).astype(np.float64)
+    kbad = (e32.astype(np.int64) - 127) != k64
+    fin = np.isfinite(Mb)
+    q64 = np.where(fin, (np.where(fin, Mb, 0) + math.log(2 / 9)) / LN2, 0.0)
+    kdist = np.abs(q64 - np.round(q64))
+    # the fp32 k_b argument is three fp32 roundings of operands below |M_b| + 2
+    kbound = 4 * U32 * (np.abs(np.where(fin, Mb, 0)) + 2) / LN2
+    tau_r, h_r = (math.log(1 / 24), 14 / math.log(24)) if lut else (tau, h)
+    kagree = np.repeat(~kbad, 32, axis=1)[:, :cols]
+    bad = (c32 != c64) & kagree
+    kk = np.repeat(k64, 32, axis=1)[:, :cols].astype(np.float64)
+    with np.errstate(invalid="ignore"):
+        mag = h_r * (np.abs(x.astype(np.float64)) + np.abs(kk) * LN2 + LN6 + abs(tau_r)) + \
+            np.abs(u64) + 2
+        udist = np.abs(u64 - np.round(u64))
+    # the contract's argument w ~ 32 (u + 1) - 1/2 is about eight fp32
+    # roundings of terms of size <= mag (in units of u)
+    ubound = 4 * U32 * mag
+    return bad, udist, ubound, kbad, kdist, kbound
+
+
+@pytest.mark.parametrize("point", ["mean", "mmlu", "balance", "lut"])
+def test_contract_vs_real_valued(orc, point):
+    """The fp32 decision contract of the oracle (the fused argument of
+    readings R-1 / R-2) against Alg. 1 evaluated step by step in fp64, at
+    every operating point of Sec. IV-A and the LUT constants of Sec. II-D.
+
+    Stated bound: a code differs only where the real u = (z - tau) h lies
+    within 4 u32 (h (|x| + |k_b| log 2 + log 6 + |tau|) + |u| + 2) of an
+    integer (a code threshold), and k_b differs only where
+    (M_b + log(2/9)) / log 2 lies within 4 u32 (|M_b| + 2) / log 2 of an
+    integer.  Checked on scores placed within +-2 ulps of every threshold and
+    every k_b boundary (where disagreements are expected, and all must sit
+    inside the bound) and on random scores (where they must be rare)."""
+    from adversarial import adversarial_scores
+    mode, (tau, h) = (orc.LUT_MODE, orc.LUT) if point == "lut" else (orc.EFQ, POINTS[point])
     rng = np.random.default_rng(7)
+    adv = adversarial_scores(rng, 600, 256, tau, h)
+    bad, udist, ubound, kbad, kdist, kbound = _contract_vs_real(orc, adv, mode, tau, h)
+    assert bad.sum() > 0                       # the set does reach the thresholds
+    assert np.all(udist[bad] <= ubound[bad]), np.max(udist[bad] / ubound[bad])
+    assert np.all(kdist[kbad] <= kbound[kbad])
     x = -rng.exponential(2.5, size=(40000, 32)).astype(np.float32)
     x[:, 0] = -rng.exponential(0.5, size=40000).astype(np.float32)
-    for lut in (False, True):
-        mode, (tau, h) = (orc.LUT_MODE, orc.LUT) if lut else (orc.EFQ, orc.MEAN)
-        c32, e32 = orc.pgen(x, mode, tau, h)
-        c64, k64, u64 = orc.pgen_real(x.astype(np.float64), lut, tau, h)
-        assert np.array_equal(e32.astype(int) - 127, k64)
-        bad = c32 != c64
-        assert bad.mean() < 1e-5
-        assert np.all(np.abs(u64[bad] - np.round(u64[bad])) < 1e-4)
+    bad, udist, ubound, kbad, kdist, kbound = _contract_vs_real(orc, x, mode, tau, h)
+    assert bad.mean() < 1e-5 and kbad.mean() < 1e-5
+    assert np.all(udist[bad] <= ubound[bad]) and np.all(kdist[kbad] <= kbound[kbad])
 
 
 def test_ln2_equivariance(orc):
@@ -550,6 +598,19 @@ def test_shift_invariance_dyadic(orc):
     assert np.max(np.abs(a[0] - b[0])) < 0.2
 
 
+def test_all_zero_codes_give_zero_output(orc):
+    """With tau above the block-max residual range [log 3/4, log 3/2) (Eq.
+    z-def: z_max = M_b - k_b log 2 - log 6 lies in that range), even the
+    block maximum gets (z - tau) h < 0, so code 0 (Eq. d8-index): every code
+    of the row is 0, l = 0, and the oracle defines O = 0."""
+    w, q, k, v = _tiny(S=128, causal=False, Hq=2, Hkv=1)
+    tau = 0.5
+    assert tau > math.log(1.5)
+    out, codes, e8, m, l = orc.attn(orc.bf16_bits(q), orc.bf16_bits(k), orc.bf16_bits(v), w.scale,
+                                    False, orc.EFQ, tau=tau, h=2.3, dump=True)
+    assert np.all(codes == 0) and np.all(l == 0.0) and np.all(out == 0.0)
+
+
 def test_l_positive_and_bounded(orc):
     """Non-negative codes make l >= 0.75 (the row maximum's contribution)."""
     w, q, k, v = _tiny(S=300, causal=True, Hq=2, Hkv=1, dist="qwen", D=128)
@@ -574,6 +635,43 @@ def test_rescaling_keeps_tiles_consistent(orc, dist):
         o512 = orc.attn(qb, kb, vb, w.scale, True, mode, bc=512)
         assert rho(o64, o512) < 0.12
     assert rho(orc.attn(qb, kb, vb, w.scale, True, orc.EXPQ, bc=64), ex) < 0.25
+
+
+# ------------------------------------------------ recurrence vs numpy twin
+TWIN_CASES = [
+    # (batch, seq_q, seq_k, heads_q, heads_kv, head_dim, causal, distribution)
+    (1, 200, 200, 4, 2, 64, True, "qwen"),
+    (2, 75, 75, 2, 1, 128, False, "normal"),
+    (1, 300, 300, 8, 2, 128, True, "qwen"),
+    (1, 100, 300, 4, 4, 64, False, "qwen_spread"),
+]
+
+
+@pytest.mark.parametrize("case", TWIN_CASES)
+@pytest.mark.parametrize("mode", ["efq", "lut", "expq", "expq6"])
+def test_recurrence_matches_numpy_twin(orc, case, mode):
+    """Alg. 2 as the C oracle runs it, against the independently written
+    numpy recurrence of oracle/twin.py (64-key tiles in ascending order,
+    Eq. (alpha) rescaling, the grouped-query head map, V~ from the twin's own
+    MXFP4 quantiser, codes from the twin's Alg. 1 or exp-then-quantize):
+    codes, E8M0 and final row maxima bit for bit, row sums within 1e-12
+    relative, outputs within one fp32 ulp.  Causal and non-causal,
+    grouped-query ratios 2 and 4, seq_q < seq_k, ragged tails."""
+    from oracle import twin
+    Bt, Sq, Sk, Hq, Hkv, D, causal, dist = case
+    w = inputs.Workload("tw", Bt, Hq, Hkv, max(Sq, Sk), D, causal, dist, 31 + Sq)
+    q, k, v = inputs.make_qkv(w)
+    q, k, v = q[:, :Sq].contiguous(), k[:, :Sk].contiguous(), v[:, :Sk].contiguous()
+    qb, kb, vb = (orc.bf16_bits(t) for t in (q, k, v))
+    om = {"efq": orc.EFQ, "lut": orc.LUT_MODE, "expq": orc.EXPQ, "expq6": orc.EXPQ6}[mode]
+    tau, h = orc.LUT if mode == "lut" else orc.MEAN
+    o1, c1, e1, m1, l1 = orc.attn(qb, kb, vb, w.scale, causal, om, tau=tau, h=h, bc=64, dump=True)
+    o2, c2, e2, m2, l2 = twin.attn_twin(qb, kb, vb, w.scale, causal, mode, tau, h, bc=64)
+    assert np.array_equal(c1, c2)
+    assert np.array_equal(e1, e2)
+    assert np.array_equal(m1, m2)
+    assert np.max(np.abs(l1 - l2) / l2) <= 1e-12
+    np.testing.assert_array_max_ulp(o1, o2, maxulp=1)
 
 
 # ------------------------------------------------------------ calibration
