@@ -547,11 +547,15 @@ struct Smem {
 };
 
 // Direct-to-LDS loads (buffer_load ... lds: LDS address = M0 base + size *
-// lane).  The buffer resource's range check returns zeros past the end of
-// K, so keys beyond seq_k need no special case (they are masked anyway).
-// The per-lane byte offsets are loop invariant; the tile position goes in
-// the scalar offset.  Asynchronous: the caller waits on vmcnt before the
-// workgroup barrier that publishes the tile.
+// lane).  The per-lane byte offsets are loop invariant; the tile position
+// goes in the scalar offset, except for the last K tile.  The buffer range
+// check compares the per-lane offset with the record count and leaves the
+// scalar offset out, so the last (possibly ragged) K tile is read through a
+// resource that starts at that tile: lanes of keys past seq_k then fall
+// outside its record count and read zeros instead of memory past the end of
+// K (those keys are masked anyway).  Every other tile lies inside K, and V~
+// and the MXFP8 K^ are padded to whole tiles.  Asynchronous: the caller
+// waits on vmcnt before the workgroup barrier that publishes the tile.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, unsigned bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
@@ -561,14 +565,16 @@ struct KLoad {
   static constexpr int KK = D / 16;
   static constexpr int PER = 2 * KK / NW;                // 1 KB blocks per wave
   static_assert(KK % PER == 0, "a wave's blocks share one 32-key window");
-  const void* base;
+  const uint8_t* base;
   unsigned bytes;
   int voff0;                                             // lane's byte offset, first block
   unsigned tile_bytes;                                   // bytes per 64 keys
+  int last;                                              // index of the last K tile
   __device__ void init(const unsigned short* kbatch, int Sk, int Hkv, int g, int wave, int lane) {
-    base = kbatch;
+    base = (const uint8_t*)kbatch;
     bytes = (unsigned)((long)Sk * Hkv * D * 2);
     tile_bytes = (unsigned)(kBc * Hkv * D * 2);
+    last = (Sk - 1) / kBc;
     // the wave's blocks are (window w, k-steps kk0 .. kk0+PER-1): block i
     // sits 32 bytes (16 bf16 columns) after block i-1 in every row
     const int blk = wave * PER;
@@ -578,11 +584,14 @@ struct KLoad {
   }
   static constexpr int kIssued = PER;                    // loads per wave per tile
   __device__ void issue(uint8_t* kbuf, int tile, int wave) const {
-    const auto rsrc = make_rsrc(base, bytes);
+    const unsigned off = (unsigned)tile * tile_bytes;
+    const bool at_end = tile == last;                    // wave-uniform
+    const auto rsrc = at_end ? make_rsrc(base + off, bytes - off) : make_rsrc(base, bytes);
+    const int soff = at_end ? 0 : (int)off;
 #pragma unroll
     for (int i = 0; i < PER; ++i)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, kbuf + (wave * PER + i) * 1024, 16,
-                                               voff0 + 32 * i, (int)(tile * tile_bytes), 0, 0);
+                                               voff0 + 32 * i, soff, 0, 0);
   }
 };
 
@@ -1344,9 +1353,11 @@ attn_pp_kernel(const void* __restrict__ q, const void* __restrict__ k,
   wait_vmem();   // no load may still target LDS when the wave leaves
 
   // O = A / l as A * (1 / l): one division per row instead of one per
-  // element (within 1.5 ulp of the quotient)
+  // element (within 1.5 ulp of the quotient).  l = 0 only when every code of
+  // the row is 0, which an operating point with tau above the block-max
+  // residual range [log 3/4, log 3/2) can produce; the row is then 0.
   const float l = w.lacc[0];
-  const float rl = 1.0f / l;
+  const float rl = l > 0.0f ? 1.0f / l : 0.0f;
   if (w.my_q < a.Sq) {
     float* op = out + (((long)b * a.Sq + w.my_q) * a.Hq + hq) * D;
 #pragma unroll
@@ -1445,6 +1456,9 @@ __global__ __launch_bounds__(256) void pgen_bench_kernel(int iters, float tau, f
   unsigned acc = 0;
   float m = -INFINITY;
   for (int it = 0; it < iters; ++it) {
+    // the scores count as changed in every iteration, so no part of the
+    // stage (block maxima, products with the scale) moves out of the loop
+    asm volatile("" : "+v"(s0), "+v"(s1));
     PgenOut po = pgen<KIND>(s0, s1, m, pa);
     acc ^= po.bop[0] ^ (po.bop[1] << 1) ^ (po.bop[2] << 2) ^ (po.bop[3] << 3) ^ (unsigned)po.scale_b;
     acc += __float_as_uint(po.alpha);
@@ -1520,6 +1534,7 @@ __global__ __launch_bounds__(256) void rho_final_kernel(const double* __restrict
 
 // ================================================================ host side
 constexpr int kQTile = kPPBr;   // queries per workgroup of the launched kernel
+constexpr int kMaxDevices = 64; // device indices the library accepts
 
 thread_local char g_msg[512] = "ok";
 
@@ -1532,13 +1547,13 @@ int fail(int status, const char* fmt, ...) {
 }
 
 std::mutex g_dev_mu;
-int g_dev_ok[64];  // 0 unknown, 1 gfx950, -1 unusable
+int g_dev_ok[kMaxDevices];  // 0 unknown, 1 gfx950, -1 unusable
 
 int check_device() {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return fail(EFQ_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
-  if (dev < 0 || dev >= 64) return fail(EFQ_EHIP, "device index %d out of range", dev);
+  if (dev < 0 || dev >= kMaxDevices) return fail(EFQ_EHIP, "device index %d out of range", dev);
   std::lock_guard<std::mutex> lk(g_dev_mu);
   if (g_dev_ok[dev] == 0) {
     hipDeviceProp_t prop;
@@ -1610,16 +1625,20 @@ int launch_vquant(const void* v, const efq_shape* s, void* vhat, hipStream_t st)
 template <int D, int KIND, bool CAUSAL, bool DUMP, bool Q8>
 hipError_t launch_attn_t(const void* q, const void* k, const void* vhat, float* out,
                          const AttnArgs& a, hipStream_t st, unsigned grid) {
-  // more dynamic LDS than the default limit: raise it once per kernel (the
-  // call is idempotent, so a race between threads is harmless)
-  static bool lds_ok = false;
-  if (!lds_ok) {
-    hipError_t e = hipFuncSetAttribute((const void*)attn_pp_kernel<D, KIND, CAUSAL, DUMP, Q8>,
+  // more dynamic LDS than the default limit: raised once per kernel and
+  // device (check_device has bounded the device index)
+  static std::once_flag once[kMaxDevices];
+  static hipError_t set_err[kMaxDevices];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::call_once(once[dev], [dev]() {
+    set_err[dev] = hipFuncSetAttribute((const void*)attn_pp_kernel<D, KIND, CAUSAL, DUMP, Q8>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
                                        SmemPP<D, Q8>::kTotal);
-    if (e != hipSuccess) return e;
-    lds_ok = true;
-  }
+  });
+  if (set_err[dev] != hipSuccess) return set_err[dev];
   constexpr int lds = SmemPP<D, Q8>::kTotal;
   hipLaunchKernelGGL((attn_pp_kernel<D, KIND, CAUSAL, DUMP, Q8>), dim3(grid), dim3(kPPThreads),
                      lds, st, q, k, (const uint8_t*)vhat, out, a);

@@ -92,7 +92,16 @@ def _unpack(codes_u8):
     return np.stack([c & 0xF, c >> 4], axis=-1).reshape(*c.shape[:-1], -1)
 
 
-@pytest.mark.parametrize("case", CASES + EDGE)
+# Deep shapes (18-24 key tiles per wave): every ring slot is refilled
+# several times.
+DEEP = [
+    (1, 1100, 1100, 8, 2, 128, True),
+    (1, 64, 1500, 4, 1, 64, False),
+    (1, 300, 1300, 2, 2, 128, False),
+]
+
+
+@pytest.mark.parametrize("case", CASES + EDGE + DEEP)
 @pytest.mark.parametrize("kind", ["efq", "lut"])
 def test_qk8_dump_exact_scores(B, orc, case, kind):
     """Dyadic Q and K (multiples of 1/2 up to 2) are exact in MXFP8 and every

@@ -12,6 +12,8 @@ import torch
 
 from paper_2609_09721_amd import inputs
 
+from adversarial import adversarial_scores
+
 pytestmark = pytest.mark.gpu
 
 TOL = 2e-3
@@ -24,46 +26,6 @@ def B():
     binding.lib()
     assert torch.cuda.is_available(), "no GPU"
     return binding
-
-
-def adversarial_scores(rng, rows, cols, tau, h):
-    """Shifted scores with exact code thresholds, k-boundaries, masked keys,
-    denormals and very negative block maxima."""
-    x = -rng.exponential(2.5, size=(rows, cols)).astype(np.float32)
-    nblk = (cols + 31) // 32
-    for r in range(rows):
-        kind = r % 6
-        for b in range(nblk):
-            t0 = b * 32
-            n = min(32, cols - t0)
-            if kind == 0:       # block max 0 -> k = -3; neighbours of every threshold
-                x[r, t0] = 0.0
-                for i in range(1, n):
-                    c = (i - 1) % 7
-                    xt = np.float32(tau + c / h - 3 * LN2 + math.log(6.0))
-                    step = (i - 1) // 7 - 2   # -2..+2 ulps
-                    v = xt
-                    for _ in range(abs(step)):
-                        v = np.nextafter(v, np.float32(np.inf if step > 0 else -np.inf))
-                    x[r, t0 + i] = min(v, np.float32(0.0))
-            elif kind == 1:     # block maxima at and around k boundaries
-                j = -3 - (b % 20)
-                Mb = np.float32(j * LN2 - math.log(2 / 9))
-                d = (r // 6 + b) % 5 - 2
-                for _ in range(abs(d)):
-                    Mb = np.nextafter(Mb, np.float32(np.inf if d > 0 else -np.inf))
-                x[r, t0] = min(Mb, np.float32(0.0))
-            elif kind == 2:     # masked keys
-                mask = rng.random(n) < 0.5
-                x[r, t0:t0 + n][mask] = -np.inf
-                if b % 3 == 0:
-                    x[r, t0:t0 + n] = -np.inf
-            elif kind == 3:     # denormals and tiny values
-                x[r, t0:t0 + n] = -rng.uniform(0, 1e-37, n).astype(np.float32)
-                x[r, t0 + 1] = -np.float32(1e-42)
-            elif kind == 4:     # block maximum below the E8M0 range
-                x[r, t0:t0 + n] -= np.float32(80 + (b % 10))
-    return x
 
 
 def unpack(codes_u8: np.ndarray) -> np.ndarray:
@@ -162,13 +124,25 @@ EDGE = [
 ]
 
 
-@pytest.mark.parametrize("case", CASES + EDGE)
+# Deep shapes: each wave streams 18-24 key tiles, so every slot of the K
+# ring (6 tiles) and the V~ ring (7 tiles) is refilled several times under
+# the four-tiles-ahead schedule: causal with grouped-query ratio 4, a
+# ragged tail past 23 full tiles, and seq_q < seq_k over 21 tiles.
+DEEP = [
+    (1, 1100, 1100, 8, 2, 128, True),
+    (1, 64, 1500, 4, 1, 64, False),
+    (1, 300, 1300, 2, 2, 128, False),
+]
+
+
+@pytest.mark.parametrize("case", CASES + EDGE + DEEP)
 @pytest.mark.parametrize("kind", ["efq", "lut"])
 def test_attn_dump_exact_scores(B, orc, case, kind):
     """Exact-score inputs: every Q.K partial sum is exact, so the fused
     kernel and the oracle see identical scores; codes and scales must match
     bit for bit, the output within tolerance."""
     Bt, Sq, Sk, Hq, Hkv, D, causal = case
+    print(f"[parity] dump {case} {kind}", flush=True)
     w = inputs.Workload("d", Bt, Hq, Hkv, max(Sq, Sk), D, causal, "dyadic", 11 + Sq)
     q, k, v = inputs.dyadic_qkv(w)
     q, k, v = q[:, :Sq].contiguous(), k[:, :Sk].contiguous(), v[:, :Sk].contiguous()
@@ -225,6 +199,20 @@ def test_single_key_returns_its_value(B):
             for h in range(2):
                 err = (out[0, 0, h].cpu() - ref).abs().max().item()
                 assert err <= 1e-6 * max(1.0, ref.abs().max().item()), (D, kind, h, err)
+
+
+def test_all_zero_codes_give_zero_output(B, orc):
+    """tau above the block-max residual range [log 3/4, log 3/2) maps every
+    score, the block maxima included, to code 0 (Eq. d8-index), so l = 0:
+    the oracle defines O = 0 for such a row and the kernel must write 0, not
+    0 * inf."""
+    w = inputs.WORKLOADS["tiny"]
+    q, k, v = inputs.make_qkv(w)
+    out = B.attn_fwd(q.cuda(), k.cuda(), v.cuda(), w.scale, False, "efq", (0.5, 2.3))
+    oo = orc.attn(orc.bf16_bits(q), orc.bf16_bits(k), orc.bf16_bits(v), w.scale, False, orc.EFQ,
+                  tau=0.5, h=2.3)
+    assert np.all(oo == 0.0)
+    assert bool(torch.isfinite(out).all()) and float(out.abs().max()) == 0.0
 
 
 def test_tiny_config_all_rows(B, orc):
