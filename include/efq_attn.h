@@ -134,6 +134,22 @@ int efq_attn_fwd_ex(const void *q, const void *k, const void *v, float scale, in
                     int kind, efq_params p, float *out, const efq_shape *s, void *ws,
                     size_t ws_bytes, efq_stream_t stream);
 
+/* efq_attn_fwd_ex without any allocation, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  V~ goes into a scratch array the library
+ * holds in device memory, EFQ_NOALLOC_SCRATCH_BYTES per GPU, for the life of
+ * the process; the caller passes inputs and output as in efq_attn_fwd_ex.
+ * Shapes whose V~ (efq_vhat_bytes) exceeds that size are rejected with
+ * EFQ_EWORKSPACE and nothing is enqueued.  The first call on a device, with
+ * that device current, looks up the array's address on the device; no call
+ * allocates or frees memory.  Every call on one GPU uses the same array, so
+ * calls that overlap in time on one GPU (different streams, or different
+ * host threads) race and must be ordered by the caller. */
+#define EFQ_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int efq_attn_fwd_noalloc(const void *q, const void *k, const void *v, float scale, int causal,
+                         int kind, efq_params p, float *out, const efq_shape *s,
+                         efq_stream_t stream);
+
 /* The two entry points of the method: EFQ-Softmax with the Mean operating
  * point, and the exp-then-quantize MXFP4 baseline. */
 int efq_attn_fwd(const void *q, const void *k, const void *v, float scale, int causal,

@@ -61,6 +61,7 @@ SIGNATURES = {
     "efq_attn_fwd_vhat": ([P, P, P, SZ, F, I, I, Params, P, SP, P], I),
     "efq_attn_fwd_ex": ([P, P, P, F, I, I, Params, P, SP, P, SZ, P], I),
     "efq_attn_fwd": ([P, P, P, F, I, P, SP, P], I),
+    "efq_attn_fwd_noalloc": ([P, P, P, F, I, I, Params, P, SP, P], I),
     "efq_attn_fwd_expq": ([P, P, P, F, I, P, SP, P], I),
     "efq_pgen": ([P, I, I, I, Params, P, P, P], I),
     "efq_attn_fwd_dump": ([P, P, P, SZ, F, I, I, Params, P, SP, P, P, P, P, P], I),
@@ -187,6 +188,23 @@ def attn_fwd(q, k, v, scale: Optional[float] = None, causal: bool = False, kind=
     _check(lib().efq_attn_fwd_ex(_ptr(q), _ptr(k), _ptr(v), float(scale), int(causal), kind,
                                  _params(kind, params), _ptr(out), ctypes.byref(sh),
                                  _ptr(workspace), ws_n, _stream(stream)))
+    return out
+
+
+def attn_fwd_noalloc(q, k, v, out: torch.Tensor, scale: Optional[float] = None,
+                     causal: bool = False, kind="efq", params=None, stream=None) -> torch.Tensor:
+    """attn_fwd through the entry point that allocates nothing (V~ in the
+    library's scratch array); out is the caller's fp32 BSHD tensor."""
+    _bf16(q, "q")
+    _bf16(k, "k")
+    _bf16(v, "v")
+    sh = shape_of(q, k)
+    kind = _kind(kind)
+    if scale is None:
+        scale = q.shape[-1] ** -0.5
+    _check(lib().efq_attn_fwd_noalloc(_ptr(q), _ptr(k), _ptr(v), float(scale), int(causal), kind,
+                                      _params(kind, params), _ptr(out), ctypes.byref(sh),
+                                      _stream(stream)))
     return out
 
 

@@ -1845,6 +1845,64 @@ int efq_attn_fwd_ex(const void* q, const void* k, const void* v, float scale, in
   return rc;
 }
 
+}  // extern "C"
+
+namespace {
+// Scratch of efq_attn_fwd_noalloc: V~ of one call.  Host code never uses the
+// array's name as an address; it uses the device address that
+// hipGetSymbolAddress returns for the current device (g_scratch).
+static __device__ __align__(256) uint8_t scratch[EFQ_NOALLOC_SCRATCH_BYTES];
+std::once_flag g_scratch_once[kMaxDevices];
+void* g_scratch[kMaxDevices];
+hipError_t g_scratch_err[kMaxDevices];
+
+// Device address of this device's scratch array (looked up once per device,
+// with that device current).
+int scratch_ptr(void** ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(EFQ_EHIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(EFQ_EHIP, "device index %d out of range", dev);
+  std::call_once(g_scratch_once[dev], [dev]() {
+    void* p = nullptr;
+    g_scratch_err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    g_scratch[dev] = p;
+  });
+  if (g_scratch_err[dev] != hipSuccess || g_scratch[dev] == nullptr)
+    return fail(EFQ_EHIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(g_scratch_err[dev]));
+  *ptr = g_scratch[dev];
+  return EFQ_OK;
+}
+}  // namespace
+
+extern "C" {
+
+int efq_attn_fwd_noalloc(const void* q, const void* k, const void* v, float scale, int causal,
+                         int kind, efq_params p, float* out, const efq_shape* s,
+                         efq_stream_t stream) {
+  int rc = validate_shape(s, causal);
+  if (rc) return rc;
+  if (!q || !k || !v || !out) return fail(EFQ_EINVAL, "null pointer");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
+    return fail(EFQ_EINVAL, "pointers must be 16-byte aligned");
+  if ((rc = check_kind(kind, true)) || (rc = check_params(p)) || (rc = check_scale(scale))) return rc;
+  const size_t need = vhat_bytes(s);
+  if (need > EFQ_NOALLOC_SCRATCH_BYTES)
+    return fail(EFQ_EWORKSPACE, "V~ needs %zu bytes, above the %zu-byte scratch of "
+                "efq_attn_fwd_noalloc (use efq_attn_fwd_ex with a workspace)",
+                need, (size_t)EFQ_NOALLOC_SCRATCH_BYTES);
+  if ((rc = check_device())) return rc;
+  void* buf = nullptr;
+  if ((rc = scratch_ptr(&buf))) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  // the V quantiser writes every byte of V~ the attention kernel reads, so
+  // nothing left by an earlier call needs clearing
+  rc = launch_vquant(v, s, buf, st);
+  if (rc == EFQ_OK)
+    rc = launch_attn(q, k, buf, scale, causal, kind, p, out, s, st, nullptr, nullptr, nullptr, nullptr);
+  return rc;
+}
+
 int efq_attn_fwd(const void* q, const void* k, const void* v, float scale, int causal, float* out,
                  const efq_shape* s, efq_stream_t stream) {
   return efq_attn_fwd_ex(q, k, v, scale, causal, EFQ_PGEN_EFQ, efq_params{EFQ_TAU_MEAN, EFQ_H_MEAN},
