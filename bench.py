@@ -3,22 +3,28 @@
 One step = the whole hot path on one batch of synthetic input already in
 HBM: V -> MXFP4 pre-pass, then the fused attention forward (bf16 Q K^T on
 MFMA, EFQ probability stage, FP4 P~V and P~1, online rescaling, final
-division).  Prints one JSON line.
+division).  The headline workload is the 32K-token Qwen3-8B-shaped causal
+prefill (32 query / 8 key-value heads, head_dim 128).  Prints one JSON line.
 
 Besides the headline TFLOP/s it reports
   * roofline: the fused attention kernel's algorithmic flops over its
     average launch time (HIP events on the launch stream), against the
-    MI355X dense bf16 / MXFP4 peaks weighted by the flop split;
+    MI355X dense bf16 / MXFP4 peaks weighted by the flop split, with the
+    kernel-trace average and the HBM traffic of the committed rocprofv3
+    summaries when they were taken on the current kernel source;
   * pgen: the probability stage alone (register-resident probe), EFQ vs
-    exp-then-quantize, in microseconds per 128x128 score tile on one CU,
-    and the exposed stage cost inside the fused kernel (policy minus a
-    no-op probability stage);
+    exp-then-quantize, in microseconds per 128x128 score tile on one CU;
+    the exposed stage cost inside the fused kernel (policy minus a no-op
+    probability stage); and the stage's VALU-active cycles from the
+    committed counter summary;
   * lowbit: the low-bit variant (MXFP8 Q and K, Q K^T on the FP8 matrix
-    core) on the same workload, its fused kernel against the FP8 / MXFP4
-    peaks, per probability stage;
-  * target and workloads: the fused kernel on the other benchmark shapes
-    (Qwen3-8B 32K and 128K, Qwen3-VL 32K, WAN2.2 75600);
-  * cpu_baseline: the CPU oracle on a bounded sample of the same workload.
+    core) on the same workload, per probability stage;
+  * workloads: the fused kernel on the other benchmark shapes (Qwen3-8B 16K
+    and 128K, Qwen3-VL 32K, WAN2.2 75600);
+  * cpu_baseline: the CPU oracle on a bounded sample of the same workload,
+    on all host threads and on one, plus the output quality
+    rho = ||O - O_exact||_F / ||O_exact||_F of the GPU's EFQ, LUT and
+    exp-then-quantize outputs on those rows against exact softmax.
 """
 from __future__ import annotations
 
@@ -57,11 +63,9 @@ def kernel_hash(src_path: str = None) -> str:
     return hashlib.sha256(code.encode()).hexdigest()[:16]
 
 
-def read_traffic(workload: str, profiles_dir: str = None):
-    """HBM bytes per launch of the attention kernel from the committed
-    rocprofv3 counter summary, if it was taken on the current kernel source."""
-    path = os.path.join(profiles_dir or os.path.join(ROOT, "profiles"),
-                        f"attn_fwd_{workload}_traffic.txt")
+def read_profile(path: str):
+    """key = value lines of a committed rocprofv3 summary, or None if the
+    summary is missing or was taken on another kernel source."""
     if not os.path.exists(path):
         return None
     kv = {}
@@ -71,10 +75,51 @@ def read_traffic(workload: str, profiles_dir: str = None):
             kv[k.strip()] = v.strip()
     if kv.get("kernel_hash") != kernel_hash():
         return None
+    return kv
+
+
+def _profiles(profiles_dir):
+    return profiles_dir or os.path.join(ROOT, "profiles")
+
+
+def read_traffic(workload: str, profiles_dir: str = None):
+    """HBM bytes per launch of the attention kernel from the committed
+    rocprofv3 counter summary, if it was taken on the current kernel source."""
+    kv = read_profile(os.path.join(_profiles(profiles_dir), f"attn_fwd_{workload}_traffic.txt"))
     try:
-        return float(kv["traffic_bytes_per_launch"])
+        return float(kv["traffic_bytes_per_launch"]) if kv else None
     except (KeyError, ValueError):
         return None
+
+
+def read_trace_avg_ms(workload: str, profiles_dir: str = None):
+    """Average and median duration (ms) of the bench-configuration EFQ
+    attention launches in the committed kernel-trace summary of this
+    workload, if it was taken on the current kernel source."""
+    kv = read_profile(os.path.join(_profiles(profiles_dir),
+                                   f"attn_pp_kernel_{workload}_stats.txt"))
+    try:
+        return (float(kv["efq_avg_us"]) / 1e3, float(kv["efq_median_us"]) / 1e3) if kv else None
+    except (KeyError, ValueError):
+        return None
+
+
+def read_stage_counters(workload: str, profiles_dir: str = None):
+    """Probability-stage VALU-active cycles per SIMD from the committed
+    counter summary (fused kernel with the EFQ, exp-then-quantize and no-op
+    stages, bf16 Q K^T): the stage's own cycles are those above the no-op
+    stage.  Returns the cycles and the saving 1 - t_EFQ / t_EXPQ, or None."""
+    kv = read_profile(os.path.join(_profiles(profiles_dir),
+                                   f"attn_pp_kernel_{workload}_counters.txt"))
+    try:
+        efq, expq, noop = (float(kv[f"valu_active_cycles_{k}"]) for k in ("efq", "expq", "noop"))
+    except (TypeError, KeyError, ValueError):
+        return None
+    se, sx = efq - noop, expq - noop
+    return {"unit": "VALU-active cycles per SIMD above the no-op stage (rocprofv3 "
+                    "SQ_ACTIVE_INST_VALU)",
+            "efq": round(se), "expq": round(sx),
+            "speedup": round(1.0 - se / sx, 4) if sx > 0 else None}
 
 
 def main():
@@ -82,13 +127,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="qwen3_8b_16k")
+    ap.add_argument("--workload", default="qwen3_8b_32k")
     ap.add_argument("--kind", default="efq", choices=["efq", "expq", "expq6", "lut"])
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-extra", action="store_true", help="skip the P-gen and policy comparisons")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU oracle time")
-    ap.add_argument("--target-workload", default="qwen3_8b_32k",
-                    help="second workload reported beside the headline one ('' to skip)")
+    ap.add_argument("--cpu-seconds", type=float, default=8.0,
+                    help="target time of one all-thread CPU oracle call")
     ap.add_argument("--sweep", action="store_true",
                     help="sequence sweep of the Qwen3-8B heads (16K..128K, causal): fused-kernel "
                          "time per probability stage, one JSON line per length")
@@ -127,15 +171,17 @@ def main():
     stream = torch.cuda.current_stream()
     params = binding.PARAMS_LUT if args.kind == "lut" else binding.PARAMS_MEAN
 
+    def prm(kind):
+        return binding.PARAMS_LUT if kind == "lut" else binding.PARAMS_MEAN
+
     def step(kind=args.kind, ev=None):
         if ev is not None:
             ev[0].record(stream)
         binding.quant_v(v, seq_q=w.seq, heads_q=w.heads_q, out=vhat, stream=stream)
         if ev is not None:
             ev[1].record(stream)
-        binding.attn_fwd_vhat(q, k, vhat, w.scale, w.causal, kind,
-                              binding.PARAMS_LUT if kind == "lut" else binding.PARAMS_MEAN,
-                              out=out, stream=stream)
+        binding.attn_fwd_vhat(q, k, vhat, w.scale, w.causal, kind, prm(kind), out=out,
+                              stream=stream)
         if ev is not None:
             ev[2].record(stream)
 
@@ -163,10 +209,10 @@ def main():
         qh, kh = binding.quant_qk(q, k, stream=stream)
         binding.quant_v(v, seq_q=w.seq, heads_q=w.heads_q, out=vhat, stream=stream)
         for kind in ("efq", "noop", "expq"):
-            prm = binding.PARAMS_MEAN
-            binding.attn_fwd_vhat(q, k, vhat, w.scale, w.causal, kind, prm, out=out, stream=stream)
-            binding.attn_fwd_qk8(qh, kh, vhat, sh, w.scale, w.causal, kind, prm, out=out,
-                                 stream=stream)
+            binding.attn_fwd_vhat(q, k, vhat, w.scale, w.causal, kind, binding.PARAMS_MEAN,
+                                  out=out, stream=stream)
+            binding.attn_fwd_qk8(qh, kh, vhat, sh, w.scale, w.causal, kind, binding.PARAMS_MEAN,
+                                 out=out, stream=stream)
         torch.cuda.synchronize()
         log(f"[bench] pmc variants done ({w.name})")
         return
@@ -192,6 +238,7 @@ def main():
     peak = 1.0 / (0.5 / PEAK_BF16 + 0.5 / PEAK_FP4)
     log(f"[bench] {args.kind}: {ms_step:.3f} ms/step (attn {attn_ms:.3f} ms, vquant {vq_ms:.3f} ms), "
         f"{value:.1f} TFLOP/s, wall {wall:.2f}s")
+    trace_ms = read_trace_avg_ms(w.name) if args.kind == "efq" else None
 
     result = {
         "metric": "attention fwd TFLOPS (EFQ-Softmax P-gen) + P-gen stage us/tile vs exp-then-quant",
@@ -222,6 +269,10 @@ def main():
             "traffic": read_traffic(w.name),
             "flops_per_launch": flops,
             "avg_launch_ms": round(attn_ms, 4),
+            "trace_avg_ms": trace_ms[0] if trace_ms else None,
+            "trace_median_ms": trace_ms[1] if trace_ms else None,
+            "trace_frac": (round(flops / (trace_ms[0] * 1e-3) / 1e12 / peak, 4)
+                           if trace_ms else None),
         },
         "vquant_ms": round(vq_ms, 4),
     }
@@ -232,7 +283,7 @@ def main():
         for kind in ("expq", "expq6", "noop", "lut"):
             if kind == args.kind:
                 continue
-            ms_k, attn_k, _, _ = timed(kind, max(5, args.steps // 2), 2)
+            _, attn_k, _, _ = timed(kind, max(5, args.steps // 2), 2)
             extra[kind] = {"attn_ms": round(attn_k, 4),
                            "tflops": round(flops / (attn_k * 1e-3) / 1e12, 2)}
         extra[args.kind] = {"attn_ms": round(attn_ms, 4), "tflops": round(achieved, 2)}
@@ -266,21 +317,28 @@ def main():
             "exposed_in_kernel": exposed,
             "exposed_speedup": (round(1.0 - exposed["efq"] / exposed["expq"], 4)
                                 if exposed.get("expq", 0) > 0 else None),
+            "stage_valu_counters": read_stage_counters(w.name),
             "paper_context": "Ascend 950PR vector-stage latency reduction 40.33% (16K-128K)",
         }
         result["policies"] = extra
-
-    if not args.no_extra:
         result["lowbit"] = lowbit_run(w, binding, q, k, v, vhat, out, stream, args.steps)
-
-    if not args.no_extra and args.target_workload:
-        result["target"] = target_run(args, binding, inputs, dev, stream)
-
-    if not args.no_extra:
-        result["workloads"] = workloads_run(binding, inputs, dev, stream)
+        result["workloads"] = workloads_run(binding, inputs, dev, stream, skip=w.name)
 
     if not args.no_cpu:
-        result["cpu_baseline"] = cpu_baseline(w, q, k, v, args.cpu_seconds)
+        # GPU outputs of the sampled rows for the quality figure, then the
+        # CPU oracle leg on the same rows
+        rows = inputs.sample_rows(w, 1024, seed=1)
+        gpu_rows = {}
+        binding.quant_v(v, seq_q=w.seq, heads_q=w.heads_q, out=vhat, stream=stream)
+        for kind in ("efq", "lut", "expq"):
+            binding.attn_fwd_vhat(q, k, vhat, w.scale, w.causal, kind, prm(kind), out=out,
+                                  stream=stream)
+            gpu_rows[kind] = out[rows[:, 0].long(), rows[:, 2].long(),
+                                 rows[:, 1].long()].cpu().numpy()
+        del vhat, out
+        torch.cuda.empty_cache()
+        result["cpu_baseline"] = cpu_baseline(w, q, k, v, args.cpu_seconds, rows.numpy(),
+                                              gpu_rows)
 
     print(json.dumps(result), flush=True)
 
@@ -386,11 +444,9 @@ def lowbit_run(w, binding, q, k, v, vhat, out, stream, steps):
     n = max(5, steps // 2)
     res = {"qk": "mxfp8 (e4m3, e8m0 per 32)", "peak": round(peak, 1), "unit": "TFLOP/s"}
     for kind in ("efq", "expq", "expq6", "noop"):
-        prm = binding.PARAMS_MEAN
-
-        def call(kind=kind, prm=prm):
-            binding.attn_fwd_qk8(qh, kh, vhat, sh, w.scale, w.causal, kind, prm, out=out,
-                                 stream=stream)
+        def call(kind=kind):
+            binding.attn_fwd_qk8(qh, kh, vhat, sh, w.scale, w.causal, kind, binding.PARAMS_MEAN,
+                                 out=out, stream=stream)
         for _ in range(2):
             call()
         torch.cuda.synchronize()
@@ -420,16 +476,18 @@ def lowbit_run(w, binding, q, k, v, vhat, out, stream, steps):
     return res
 
 
-def workloads_run(binding, inputs, dev, stream):
-    """The other benchmark shapes (Qwen3-8B 128K causal, Qwen3-VL 32K and
-    WAN2.2 75600 non-causal): fused-kernel time (median of 3 launches) per
-    probability stage, bf16 and MXFP8 Q K^T, and the fraction of each
+def workloads_run(binding, inputs, dev, stream, skip=None):
+    """The other benchmark shapes (Qwen3-8B 16K and 128K causal, Qwen3-VL 32K
+    and WAN2.2 75600 non-causal): fused-kernel time (median of 3 launches)
+    per probability stage, bf16 and MXFP8 Q K^T, and the fraction of each
     path's MFMA roofline."""
     import torch
     peak = 1.0 / (0.5 / PEAK_BF16 + 0.5 / PEAK_FP4)
     peak8 = 1.0 / (0.5 / PEAK_FP8 + 0.5 / PEAK_FP4)
     res = {"timing": "median of 3 launches after one warm-up"}
-    for name in ("qwen3_8b_128k", "qwen3_vl_32k", "wan22_75600"):
+    for name in ("qwen3_8b_16k", "qwen3_8b_128k", "qwen3_vl_32k", "wan22_75600"):
+        if name == skip:
+            continue
         w = inputs.WORKLOADS[name]
         q, k, v = inputs.make_qkv(w, device=dev)
         vh = binding.quant_v(v, seq_q=w.seq, heads_q=w.heads_q, stream=stream)
@@ -459,53 +517,17 @@ def workloads_run(binding, inputs, dev, stream):
     return res
 
 
-def target_run(args, binding, inputs, dev, stream):
-    """The fused kernel on a second workload (the 32K-token Qwen3-8B heads),
-    timed like the headline one; attention kernel only."""
-    import torch
-    w = inputs.WORKLOADS[args.target_workload]
-    q, k, v = inputs.make_qkv(w, device=dev)
-    vh = binding.quant_v(v, seq_q=w.seq, heads_q=w.heads_q, stream=stream)
-    out = torch.empty(q.shape, dtype=torch.float32, device=dev)
-    res = {"workload": w.name, "seq": w.seq, "causal": w.causal, "timing": "median of 10 launches"}
-    peak = 1.0 / (0.5 / PEAK_BF16 + 0.5 / PEAK_FP4)
-    for kind in ("efq", "expq"):
-        prm = binding.PARAMS_MEAN
-
-        def call(kind=kind, prm=prm):
-            binding.attn_fwd_vhat(q, k, vh, w.scale, w.causal, kind, prm, out=out, stream=stream)
-        for _ in range(3):
-            call()
-        torch.cuda.synchronize()
-        ms = _median_call(call, 10, stream)
-        tf = w.flops() / (ms * 1e-3) / 1e12
-        res[kind] = {"attn_ms": round(ms, 4), "tflops": round(tf, 2), "frac": round(tf / peak, 4)}
-    # the low-bit variant (MXFP8 Q K^T) of the EFQ kernel
-    sh = binding.shape_of(q, k)
-    qh, kh = binding.quant_qk(q, k, stream=stream)
-    peak8 = 1.0 / (0.5 / PEAK_FP8 + 0.5 / PEAK_FP4)
-
-    def call():
-        binding.attn_fwd_qk8(qh, kh, vh, sh, w.scale, w.causal, "efq", binding.PARAMS_MEAN,
-                             out=out, stream=stream)
-    for _ in range(3):
-        call()
-    torch.cuda.synchronize()
-    ms = _median_call(call, 10, stream)
-    tf = w.flops() / (ms * 1e-3) / 1e12
-    res["lowbit_efq"] = {"attn_ms": round(ms, 4), "tflops": round(tf, 2),
-                         "frac": round(tf / peak8, 4), "peak": round(peak8, 1)}
-    del q, k, v, vh, out, qh, kh
-    torch.cuda.empty_cache()
-    return res
-
-
-def cpu_baseline(w, q, k, v, target_s: float):
-    """The CPU oracle (unchanged) on a stratified sample of query rows; the
-    rate is algorithmic flops of the sampled rows over the wall time of the
-    call.  Each call also quantises all of V, so the sample grows (at most
-    16x per round) until one call takes at least half the time target; the
-    reported rate is that of the last call."""
+def cpu_baseline(w, q, k, v, target_s: float, rows, gpu_rows):
+    """The CPU oracle (unchanged) on a stratified sample of query rows: the
+    rate is algorithmic flops of the sampled rows over the wall time of one
+    call, on all the host threads this job may use (at most 16) and on one
+    thread.  Each call also quantises all of V.  The sample grows (at most
+    16x per round) until the all-thread call takes at least half the time
+    target; the one-thread call gets a subsample sized to take about as
+    long.  Also the output quality on the first 1024-row sample:
+    rho = ||O - O_exact||_F / ||O_exact||_F (Sec. III-C's objective) of the
+    GPU outputs of EFQ, EFQ-Softmax-LUT and exp-then-quantize against the
+    oracle's exact fp64 softmax with unquantised V."""
     import numpy as np
     import oracle
     from paper_2609_09721_amd import inputs
@@ -514,32 +536,54 @@ def cpu_baseline(w, q, k, v, target_s: float):
     qb = oracle.bf16_bits(q)
     kb = oracle.bf16_bits(k)
     vb = oracle.bf16_bits(v)
-    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
-    cores = max(1, min(cores, 16))
+    host = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    threads = max(1, min(host, 16))
     total_rows = w.batch * w.heads_q * w.seq
 
-    def row_flops(rows):
-        keys = (rows[:, 2].astype(np.int64) + 1) if w.causal else np.full(len(rows), w.seq)
+    def row_flops(rs):
+        keys = (rs[:, 2].astype(np.int64) + 1) if w.causal else np.full(len(rs), w.seq)
         return float(4 * w.head_dim * keys.sum())
 
-    n, spent, seed = 64, 0.0, 1
-    while True:
-        rows = inputs.sample_rows(w, n, seed=seed).numpy()
+    def call(rs, nth):
         t = time.perf_counter()
-        oracle.attn(qb, kb, vb, w.scale, w.causal, oracle.EFQ, bc=64, rows=rows, nthreads=cores)
+        oracle.attn(qb, kb, vb, w.scale, w.causal, oracle.EFQ, bc=64, rows=rs, nthreads=nth)
         dt = time.perf_counter() - t
+        log(f"[bench] cpu oracle: {len(rs)} rows in {dt:.2f}s on {nth} threads")
+        return dt
+
+    # quality against exact softmax on the given rows
+    exact = oracle.attn(qb, kb, vb, w.scale, w.causal, oracle.EXACT, bc=64, rows=rows,
+                        nthreads=threads).astype(np.float64)
+    norm = np.sqrt(np.sum(exact * exact))
+    rho = {kind: round(float(np.sqrt(np.sum((o.astype(np.float64) - exact) ** 2)) / norm), 6)
+           for kind, o in gpu_rows.items()}
+
+    n, seed, spent = 64, 2, 0.0
+    while True:
+        rs = inputs.sample_rows(w, n, seed=seed).numpy()
+        dt = call(rs, threads)
         spent += dt
-        log(f"[bench] cpu oracle: {len(rows)} rows in {dt:.2f}s on {cores} threads")
         if dt >= 0.5 * target_s or n >= total_rows or spent >= 3 * target_s:
             break
         n = int(min(total_rows, n * min(16.0, max(2.0, target_s / max(dt, 1e-3)))))
         seed += 1
-    rate = row_flops(rows) / dt
-    return {"value": round(rate / 1e12, 8), "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
-            "sample": f"{len(rows)} of {total_rows} query rows of the same workload, stratified "
-                      f"over heads and positions; one call of {dt:.1f}s (includes quantising "
-                      f"all of V)",
-            "seconds": round(dt, 2)}
+    rate = row_flops(rs) / dt
+    # one thread: a subsample expected to take about as long as the call above
+    sub = rs[:: max(1, threads)]
+    dt1 = call(sub, 1)
+    rate1 = row_flops(sub) / dt1
+    return {"value": round(rate / 1e12, 8), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"{len(rs)} of {total_rows} query rows of the same workload, stratified "
+                      f"over heads and positions; one call of {dt:.1f}s on {threads} threads "
+                      f"(includes quantising all of V)",
+            "seconds": round(dt, 2),
+            "host_cores": host,
+            "single_thread": {"value": round(rate1 / 1e12, 8), "unit": "TFLOP/s", "cores": 1,
+                              "rows": len(sub), "seconds": round(dt1, 2)},
+            "rho_vs_exact": dict(rho, rows=len(rows),
+                                 definition="||O - O_exact||_F / ||O_exact||_F over the sampled "
+                                            "rows; O_exact = fp64 softmax attention with "
+                                            "unquantised V (oracle EXACT mode)")}
 
 
 if __name__ == "__main__":

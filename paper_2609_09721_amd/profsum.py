@@ -9,21 +9,27 @@ traffic FETCH_DIR WRITE_DIR WORKLOAD [OUT_FILE]
     profiles/attn_fwd_<workload>_traffic.txt, which bench.py reports as
     roofline.traffic while the kernel source is unchanged.
 
-stats TRACE_DIR OUT_FILE COMMAND...
+stats TRACE_DIR OUT_FILE WORKLOAD COMMAND...
     Kernel-time summary of a `rocprofv3 --kernel-trace --stats` run: the
     per-kernel statistics, and per launch configuration (grid size) the
-    calls and average duration of the attention kernels.
+    calls and average duration of the attention kernels.  Records the
+    average of the bf16 EFQ attention kernel at WORKLOAD's launch
+    configuration (efq_avg_us) with the kernel-source hash, which bench.py
+    reports beside its own HIP-event average.
 
 sweep JSONL OUT_FILE COMMAND...
     Table of a `bench.py --sweep` run (one JSON line per sequence length).
 
-counters PMC_DIR OUT_FILE COMMAND...
-    Per attention-kernel variant of a `bench.py --pmc-variants` run with
-    SQ_VALU_MFMA_BUSY_CYCLES, SQ_ACTIVE_INST_VALU, SQ_INSTS_VALU,
-    SQ_INSTS_MFMA, SQ_INSTS_LDS, SQ_LDS_BANK_CONFLICT and GRBM_GUI_ACTIVE:
-    matrix-core busy and VALU-active cycles per SIMD as fractions of the
-    kernel's cycles, VALU instructions per SIMD and per score, and LDS
-    bank-conflict stall cycles per LDS instruction.
+counters OUT_FILE WORKLOAD COMMAND... -- PMC_DIR [PMC_DIR ...]
+    Per attention-kernel variant of `bench.py --pmc-variants` runs (one
+    directory per counter pass, merged by dispatch order): matrix-core busy,
+    VALU-active and co-execution cycles per SIMD as fractions of the
+    kernel's cycles, VALU / MFMA / SALU / LDS instructions per SIMD and VALU
+    instructions per score, LDS bank conflicts, and, where the passes hold
+    them, the wave wait counters.  Records the VALU-active cycles per SIMD
+    of the bf16 EFQ, exp-then-quantize and no-op kernels with the
+    kernel-source hash, which bench.py reads as the probability stage's
+    counter view.
 """
 from __future__ import annotations
 
@@ -58,7 +64,15 @@ def mean_of(disp, pred):
     return sum(vals) / len(vals), len(vals)
 
 
-def stats(trace_dir: str, out: str, command: str):
+def _grid_items(workload: str) -> int:
+    """Work-items of the attention launch of a workload (256 queries and 512
+    threads per workgroup)."""
+    from paper_2609_09721_amd import inputs
+    w = inputs.WORKLOADS[workload]
+    return w.batch * w.heads_q * ((w.seq + 255) // 256) * 512
+
+
+def stats(trace_dir: str, out: str, workload: str, command: str):
     rows = []
     for f in glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True):
         rows += list(csv.DictReader(open(f)))
@@ -90,6 +104,17 @@ def stats(trace_dir: str, out: str, command: str):
             med = sorted(ds)[len(ds) // 2]
             fh.write(f"{n} | {g} | {len(ds)} | {sum(ds) / len(ds):.1f} | {med:.1f} | "
                      f"{min(ds):.1f} | {max(ds):.1f}\n")
+        import bench
+        grid = str(_grid_items(workload))
+        efq = [ds for (n, g), ds in groups.items()
+               if n == "attn_pp_kernel<128, 0, true, false, false>" and g == grid]
+        if efq:
+            ds = efq[0]
+            fh.write(f"# bf16 EFQ attention kernel at the {workload} launch configuration "
+                     f"(grid {grid})\n")
+            fh.write(f"efq_calls = {len(ds)}\nefq_avg_us = {sum(ds) / len(ds):.1f}\n")
+            fh.write(f"efq_median_us = {sorted(ds)[len(ds) // 2]:.1f}\n")
+            fh.write(f"kernel_hash = {bench.kernel_hash()}\n")
     print(open(out).read())
 
 
@@ -116,57 +141,80 @@ def sweep(jsonl: str, out: str, command: str):
     print(open(out).read())
 
 
-def counters(d: str, out: str, command: str):
+def counters(dirs, out: str, workload: str, command: str):
     import collections
-    rows = []
-    for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
-        rows += list(csv.DictReader(open(f)))
     acc = collections.defaultdict(lambda: collections.defaultdict(float))
     names = {}
-    for r in rows:
-        n = r["Kernel_Name"]
-        if "attn_pp_kernel" not in n:
-            continue
-        key = int(r["Dispatch_Id"])
-        names[key] = n.replace("(anonymous namespace)::", "").replace("void ", "").split("(")[0]
-        acc[key][r["Counter_Name"]] += float(r["Counter_Value"])
+    for d in dirs:
+        rows = []
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            rows += list(csv.DictReader(open(f)))
+        order = sorted({int(r["Dispatch_Id"]) for r in rows if "attn_pp_kernel" in r["Kernel_Name"]})
+        pos = {dsp: i for i, dsp in enumerate(order)}
+        for r in rows:
+            n = r["Kernel_Name"]
+            if "attn_pp_kernel" not in n:
+                continue
+            key = pos[int(r["Dispatch_Id"])]
+            names[key] = n.replace("(anonymous namespace)::", "").replace("void ", "").split("(")[0]
+            acc[key][r["Counter_Name"]] += float(r["Counter_Value"])
     simds, xcds = 1024, 8
     from paper_2609_09721_amd import inputs
-    pairs = inputs.WORKLOADS["qwen3_8b_16k"].pairs()
+    pairs = inputs.WORKLOADS[workload].pairs()
+    kinds = {"attn_pp_kernel<128, 0, true, false, false>": "efq",
+             "attn_pp_kernel<128, 1, true, false, false>": "expq",
+             "attn_pp_kernel<128, 3, true, false, false>": "noop"}
     with open(out, "w") as fh:
-        fh.write("# matrix-core and VALU activity of the fused attention kernel, qwen3_8b_16k\n")
-        fh.write(f"# command (from the repository root, TMPDIR=/tmp):\n#   {command}\n")
+        fh.write(f"# matrix-core and VALU activity of the fused attention kernel, {workload}\n")
+        fh.write(f"# command (from the repository root, TMPDIR=/tmp), one run per counter pass:\n")
+        for c in command.split(" ;; "):
+            fh.write(f"#   {c}\n")
         fh.write("# kernel template: <head_dim, pgen kind (0 EFQ, 1 EXPQ, 3 no-op), causal, dump, "
                  "MXFP8 Q K^T>\n")
         fh.write("# cycles per XCD = GRBM_GUI_ACTIVE / 8; MFMA busy and VALU active are per SIMD "
                  "(SQ_ACTIVE_INST_VALU is in quad-cycles, summed over the SIMD's waves)\n")
-        fh.write("# VALU per score: wave instructions x 64 lanes / visible (query, key) pairs\n")
+        fh.write("# VALU per score: wave instructions (MFMA included) x 64 lanes / visible "
+                 "(query, key) pairs\n")
         fh.write("# co-exec: cycles in which the matrix core was busy and a VALU instruction "
                  "issued (SQ_VALU_MFMA_COEXEC_CYCLES), per SIMD\n")
-        fh.write("# kernel | cycles | MFMA busy / cycles | VALU active / cycles | "
-                 "(MFMA + VALU) / cycles | co-exec / cycles | VALU instr per SIMD | "
-                 "MFMA instr per SIMD | VALU per score | LDS instr per SIMD | "
-                 "bank-conflict cycles per LDS instr\n")
+        fh.write("# wait / wait-issue: wave cycles waiting on a dependency or counter "
+                 "(SQ_WAIT_ANY) and with an instruction ready but not issued "
+                 "(SQ_WAIT_INST_ANY), per SIMD cycle, summed over the SIMD's waves\n")
+        fh.write("# kernel | cycles | MFMA busy | VALU active | co-exec | wait | wait-issue | "
+                 "VALU instr per SIMD | MFMA instr per SIMD | SALU instr per SIMD | "
+                 "VALU per score | LDS instr per SIMD | bank-conflict cycles per LDS instr\n")
+        per_kind = {}
         for key in sorted(acc):
             c = acc[key]
-            cyc = c["GRBM_GUI_ACTIVE"] / xcds
-            mf = c["SQ_VALU_MFMA_BUSY_CYCLES"] / simds
-            va = 4 * c["SQ_ACTIVE_INST_VALU"] / simds
-            co = c.get("SQ_VALU_MFMA_COEXEC_CYCLES", float("nan")) / simds
-            fh.write(f"{names[key]} | {cyc:.0f} | {mf / cyc:.3f} | {va / cyc:.3f} | "
-                     f"{(mf + va) / cyc:.3f} | {co / cyc:.3f} | {c['SQ_INSTS_VALU'] / simds:.0f} | "
-                     f"{c['SQ_INSTS_MFMA'] / simds:.0f} | {c['SQ_INSTS_VALU'] * 64 / pairs:.2f} | "
-                     f"{c.get('SQ_INSTS_LDS', 0) / simds:.0f} | "
+            cyc = c["GRBM_GUI_ACTIVE"] / xcds / max(1, len(dirs))
+            g = lambda n, scale=1.0: (c[n] * scale / simds / cyc) if n in c else float("nan")
+            va = 4 * c.get("SQ_ACTIVE_INST_VALU", float("nan")) / simds
+            fh.write(f"{names[key]} | {cyc:.0f} | {g('SQ_VALU_MFMA_BUSY_CYCLES'):.3f} | "
+                     f"{va / cyc:.3f} | {g('SQ_VALU_MFMA_COEXEC_CYCLES'):.3f} | "
+                     f"{g('SQ_WAIT_ANY', 4):.3f} | {g('SQ_WAIT_INST_ANY', 4):.3f} | "
+                     f"{c.get('SQ_INSTS_VALU', float('nan')) / simds:.0f} | "
+                     f"{c.get('SQ_INSTS_MFMA', float('nan')) / simds:.0f} | "
+                     f"{c.get('SQ_INSTS_SALU', float('nan')) / simds:.0f} | "
+                     f"{c.get('SQ_INSTS_VALU', float('nan')) * 64 / pairs:.2f} | "
+                     f"{c.get('SQ_INSTS_LDS', float('nan')) / simds:.0f} | "
                      f"{c.get('SQ_LDS_BANK_CONFLICT', 0) / max(c.get('SQ_INSTS_LDS', 0), 1):.4f}\n")
+            if names[key] in kinds:
+                per_kind[kinds[names[key]]] = (va, g("SQ_VALU_MFMA_BUSY_CYCLES"))
+        for kind, (va, mf) in sorted(per_kind.items()):
+            fh.write(f"valu_active_cycles_{kind} = {va:.0f}\nmfma_busy_{kind} = {mf:.4f}\n")
+        import bench
+        fh.write(f"kernel_hash = {bench.kernel_hash()}\n")
     print(open(out).read())
 
 
 def main():
     if sys.argv[1] == "counters":
-        counters(sys.argv[2], sys.argv[3], " ".join(sys.argv[4:]))
+        rest = sys.argv[4:]
+        cut = rest.index("--")
+        counters(rest[cut + 1:], sys.argv[2], sys.argv[3], " ".join(rest[:cut]))
         return
     if sys.argv[1] == "stats":
-        stats(sys.argv[2], sys.argv[3], " ".join(sys.argv[4:]))
+        stats(sys.argv[2], sys.argv[3], sys.argv[4], " ".join(sys.argv[5:]))
         return
     if sys.argv[1] == "sweep":
         sweep(sys.argv[2], sys.argv[3], " ".join(sys.argv[4:]))
@@ -196,9 +244,9 @@ def main():
         fh.write(f"# HBM traffic of one attention launch, {wl} (EFQ), from rocprofv3 counters\n")
         fh.write("# commands (from the repository root, TMPDIR=/tmp):\n")
         fh.write("#   rocprofv3 --pmc FETCH_SIZE -d <FETCH_DIR> -o p --output-format csv -- "
-                 "python3 bench.py --pmc-run\n")
+                 f"python3 bench.py --pmc-run --workload {wl}\n")
         fh.write("#   rocprofv3 --pmc WRITE_SIZE -d <WRITE_DIR> -o p --output-format csv -- "
-                 "python3 bench.py --pmc-run\n")
+                 f"python3 bench.py --pmc-run --workload {wl}\n")
         fh.write(f"#   python3 -m paper_2609_09721_amd.profsum traffic <FETCH_DIR> <WRITE_DIR> {wl}\n")
         fh.write(f"# attention dispatches {na}, copy dispatches {nc}; copy size {bench.COPY_BYTES} B\n")
         fh.write(f"fetch_counter_attn = {fa:.1f}\nfetch_counter_copy = {fc:.1f}\n")

@@ -44,3 +44,21 @@ def test_traffic_only_for_matching_source(tmp_path):
     f.write_text("traffic_bytes_per_launch = 123456\nkernel_hash = 0000000000000000\n")
     assert bench.read_traffic("w", str(d)) is None
     assert bench.read_traffic("missing", str(d)) is None
+
+
+def test_trace_and_counter_views_only_for_matching_source(tmp_path):
+    d = tmp_path / "profiles"
+    d.mkdir()
+    h = bench.kernel_hash()
+    (d / "attn_pp_kernel_w_stats.txt").write_text(
+        f"# trace\nefq_calls = 3\nefq_avg_us = 5400.0\nefq_median_us = 5350.0\nkernel_hash = {h}\n")
+    assert bench.read_trace_avg_ms("w", str(d)) == (5.4, 5.35)
+    (d / "attn_pp_kernel_w_counters.txt").write_text(
+        "valu_active_cycles_efq = 600\nvalu_active_cycles_expq = 900\n"
+        f"valu_active_cycles_noop = 100\nkernel_hash = {h}\n")
+    c = bench.read_stage_counters("w", str(d))
+    assert (c["efq"], c["expq"]) == (500, 800) and c["speedup"] == round(1 - 500 / 800, 4)
+    for f in d.iterdir():
+        f.write_text(f.read_text().replace(h, "0000000000000000"))
+    assert bench.read_trace_avg_ms("w", str(d)) is None
+    assert bench.read_stage_counters("w", str(d)) is None
