@@ -584,10 +584,14 @@ struct KLoad {
   }
   static constexpr int kIssued = PER;                    // loads per wave per tile
   __device__ void issue(uint8_t* kbuf, int tile, int wave) const {
-    const unsigned off = (unsigned)tile * tile_bytes;
-    const bool at_end = tile == last;                    // wave-uniform
-    const auto rsrc = at_end ? make_rsrc(base + off, bytes - off) : make_rsrc(base, bytes);
-    const int soff = at_end ? 0 : (int)off;
+    if (tile == last) {                                  // wave-uniform
+      const unsigned off = (unsigned)tile * tile_bytes;
+      put(kbuf, make_rsrc(base + off, bytes - off), 0, wave);
+    } else {
+      put(kbuf, make_rsrc(base, bytes), (int)(tile * tile_bytes), wave);
+    }
+  }
+  __device__ void put(uint8_t* kbuf, __amdgpu_buffer_rsrc_t rsrc, int soff, int wave) const {
 #pragma unroll
     for (int i = 0; i < PER; ++i)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, kbuf + (wave * PER + i) * 1024, 16,
@@ -599,28 +603,29 @@ template <int D, int NW>
 struct VLoad {
   static constexpr int kVc = Smem<D, 1, 1>::kVc;         // V~ code bytes per tile
   static constexpr int NB = kVc / 1024;                  // 1 KB code blocks (2 or 4)
+  static_assert(NB < NW, "a wave left over for the scales");
   const uint8_t* codes;
   const uint8_t* scales;
   int nb;
-  __device__ void init(const uint8_t* vcodes, const uint8_t* vscales, int nblocks) {
+  int soff_lane;                                         // lane's byte offset of the scale load
+  __device__ void init(const uint8_t* vcodes, const uint8_t* vscales, int nblocks, int lane) {
     codes = vcodes;
     scales = vscales;
     nb = nblocks;
+    // 2 D scale bytes as dwords; for D = 64 the upper lanes repeat the
+    // lower ones into the padding
+    soff_lane = (lane % (2 * D / 4)) * 4;
   }
-  // loads a wave issues per tile
-  __device__ static int issued(int wave) { return (wave < NB ? 1 : 0) + (wave == NW - 1 ? 1 : 0); }
-  __device__ void issue(uint8_t* vbuf, int tile, int wave, int lane) const {
-    const auto rc = make_rsrc(codes, (unsigned)(nb * D * 16));
-    const auto rs = make_rsrc(scales, (unsigned)(nb * D));
-    if (wave < NB)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rc, vbuf + wave * 1024, 16, lane * 16,
-                                               tile * 2 * D * 16 + wave * 1024, 0, 0);
-    if (wave == NW - 1) {
-      // 2 D scale bytes as dwords; for D = 64 the upper lanes repeat the
-      // lower ones into the padding
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, vbuf + kVc, 4, (lane % (2 * D / 4)) * 4,
-                                               tile * 2 * D, 0, 0);
-    }
+  // code block `wave` (waves below NB)
+  __device__ void issue_codes(uint8_t* vbuf, int tile, int wave, int lane) const {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(codes, (unsigned)(nb * D * 16)),
+                                             vbuf + wave * 1024, 16, lane * 16,
+                                             tile * 2 * D * 16 + wave * 1024, 0, 0);
+  }
+  // the tile's scales; several waves may load them (same bytes, same place)
+  __device__ void issue_scales(uint8_t* vbuf, int tile) const {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(scales, (unsigned)(nb * D)), vbuf + kVc, 4,
+                                             soff_lane, tile * 2 * D, 0, 0);
   }
 };
 
@@ -638,7 +643,6 @@ struct KLoad8 {
   static constexpr int NC = D / 64;                      // 64-column chunks
   static constexpr int NBLK = 4 * NC;                    // 1 KB code blocks per tile
   static_assert(NBLK <= NW, "one code block per wave");
-  static constexpr int SW = NW - 2;                      // the wave that loads the scales
   const void* codes;
   const void* scales;
   unsigned cbytes, sbytes;
@@ -652,16 +656,20 @@ struct KLoad8 {
     const int h = blk & 1, c = (blk >> 1) % NC, w = blk / (2 * NC);
     voff = (32 * w + (lane & 31)) * D + 64 * c + 32 * h + 16 * (lane >> 5);
   }
-  __device__ static int issued(int wave) { return (wave < NBLK ? 1 : 0) + (wave == SW ? 1 : 0); }
-  __device__ void issue(uint8_t* kbuf, int tile, int wave, int lane) const {
-    if (wave < NBLK)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(codes, cbytes), kbuf + wave * 1024, 16,
-                                               voff, tile * kBc * D, 0, 0);
-    // 64 keys x D/32 bytes as dwords; for D = 64 the upper lanes read the
-    // next tile's scales (or zeros past the end) into the unused half
-    if (wave == SW)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(scales, sbytes), kbuf + kBc * D, 4,
-                                               lane * 4, tile * kBc * (D / 32), 0, 0);
+  // code block `wave` (waves below NBLK)
+  __device__ void issue_codes(uint8_t* kbuf, int tile, int wave) const {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(codes, cbytes), kbuf + wave * 1024, 16,
+                                             voff, tile * kBc * D, 0, 0);
+  }
+  // 64 keys x D/32 bytes as dwords; for D = 64 the upper lanes read the
+  // next tile's scales into the unused half.  The resource starts at the
+  // tile, so the range check (which covers the per-lane offset only) turns
+  // a read past the last tile into zeros.  Several waves may load them
+  // (same bytes, same place).
+  __device__ void issue_scales(uint8_t* kbuf, int tile, int lane) const {
+    const unsigned off = (unsigned)tile * (kBc * (D / 32));
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc((const uint8_t*)scales + off, sbytes - off),
+                                             kbuf + kBc * D, 4, lane * 4, 0, 0, 0);
   }
 };
 
@@ -703,17 +711,21 @@ __device__ __forceinline__ void wait_vmem_le(int n) {
 
 // Map a workgroup index to (batch, head, query tile).  Workgroups are handed
 // to the 8 XCDs round-robin; with xcd_remap each XCD gets a contiguous range
-// of work items, so the query tiles that share a key/value head run on one
-// XCD and share its L2.  Within a head, query tiles run longest first.
+// of work items.  Consecutive work items are the query heads of one GQA group
+// at one query tile, then the next tile, so the workgroups that stream the
+// same key/value tiles run side by side on one XCD and share its L2.  Query
+// tiles run longest first.
 __device__ __forceinline__ void map_work(const AttnArgs& a, int& b, int& hq, int& qt) {
   const int n = blockIdx.x;
   const int total = gridDim.x;
   int w = n;
   if (a.xcd_remap) w = (n & 7) * (total >> 3) + (n >> 3);
-  const int bh = w / a.nqt;
-  qt = a.nqt - 1 - (w % a.nqt);
-  hq = bh % a.Hq;
-  b = bh / a.Hq;
+  const int G = a.Hq / a.Hkv;
+  const int per = G * a.nqt;          // work items of one (batch, kv head)
+  const int bg = w / per, r = w % per;
+  qt = a.nqt - 1 - r / G;
+  hq = (bg % a.Hkv) * G + r % G;
+  b = bg / a.Hkv;
 }
 
 // V~ operands of one tile for the lane: the 16 code bytes of each slab and
@@ -723,6 +735,14 @@ struct VOps {
   u32x4 a[D / 32];
   int sv;
 };
+
+// LDS addresses as 32-bit values: the lane's read addresses in ring slot 0
+// stay in registers, and a slot is one scalar offset away.
+typedef __attribute__((address_space(3))) const uint8_t* lds_cptr;
+__device__ __forceinline__ unsigned lds_addr(const void* p) {
+  return (unsigned)(uintptr_t)(lds_cptr)p;
+}
+__device__ __forceinline__ lds_cptr lds_at(unsigned a) { return (lds_cptr)(uintptr_t)a; }
 
 // Lane offsets of the V~ operand reads within a ring slot: codes, scales.
 template <int D>
@@ -734,19 +754,16 @@ __device__ __forceinline__ int vscale_offset(int lane) {
   return Smem<D, 1, 1>::kVc + (lane >> 5) * D + (lane & 31) * (D / 32);
 }
 
+// vc, vs: the lane's code and scale reads in the tile's ring slot (the slab
+// reads take immediate offsets from vc).
 template <int D>
-__device__ __forceinline__ void read_v(const uint8_t* vb, int voff, int vsoff, VOps<D>& v) {
+__device__ __forceinline__ void read_v(lds_cptr vc, lds_cptr vs, VOps<D>& v) {
   constexpr int NS = D / 32;
-  // one address per slot: the slab reads take immediate offsets from it
-  typedef __attribute__((address_space(3))) const uint8_t* lds_cptr;
-  lds_cptr vc = (lds_cptr)(vb + voff);
-  asm volatile("" : "+v"(vc));
 #pragma unroll
   for (int s = 0; s < NS; ++s)
     v.a[s] = *(__attribute__((address_space(3))) const u32x4*)(vc + s * 32 * 16);
-  const uint8_t* vsp = vb + vsoff;
-  if constexpr (NS == 4) v.sv = *(const int*)vsp;
-  else v.sv = *(const unsigned short*)vsp;
+  if constexpr (NS == 4) v.sv = *(__attribute__((address_space(3))) const int*)vs;
+  else v.sv = *(__attribute__((address_space(3))) const unsigned short*)vs;
 }
 
 // O^T slabs += V~^T P~^T on the FP4 MFMA.  The lane's E8M0 scales of all
@@ -861,7 +878,7 @@ __device__ __forceinline__ f32x4 rowsum_mfma(const i32x8& sel, const i32x8& b8, 
 #endif
 constexpr int kQkPD = EFQ_QK_PD;   // bf16 K operand reads kept this many k-steps ahead
 template <int D, int KIND, bool QK, int I>
-__device__ __forceinline__ void mc_regions(const uint8_t* p0, const uint8_t* p1, bf16x8* a0,
+__device__ __forceinline__ void mc_regions(lds_cptr p0, lds_cptr p1, bf16x8* a0,
                                            bf16x8* a1, const bf16x8* qreg, f32x16& sn0,
                                            f32x16& sn1, const f32x16& sc0, const f32x16& sc1,
                                            const PgenArgs& pa, PgenState& st) {
@@ -872,8 +889,8 @@ __device__ __forceinline__ void mc_regions(const uint8_t* p0, const uint8_t* p1,
       sn0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[I], qreg[I], sn0, 0, 0, 0);
       sn1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[I], qreg[I], sn1, 0, 0, 0);
       if constexpr (I + PD < KK) {
-        a0[I + PD] = *(const bf16x8*)(p0 + (I + PD) * 1024);
-        a1[I + PD] = *(const bf16x8*)(p1 + (I + PD) * 1024);
+        a0[I + PD] = *(__attribute__((address_space(3))) const bf16x8*)(p0 + (I + PD) * 1024);
+        a1[I + PD] = *(__attribute__((address_space(3))) const bf16x8*)(p1 + (I + PD) * 1024);
       }
     }
     constexpr int P0 = 16 * I / KK, P1 = 16 * (I + 1) / KK;
@@ -886,15 +903,15 @@ __device__ __forceinline__ void mc_regions(const uint8_t* p0, const uint8_t* p1,
 template <int D, bool Q8>
 struct KPre;
 
+// p0: the lane's operand slot in the K tile (tile base + 16 lane)
 template <int D, int KIND, bool QK, bool CODES, bool PRE>
-__device__ __forceinline__ PgenOut mma_phase(const uint8_t* kbuf, const bf16x8* qreg,
-                                             const KPre<D, false>& kp, int lane, f32x16& sn0,
+__device__ __forceinline__ PgenOut mma_phase(lds_cptr p0, const bf16x8* qreg,
+                                             const KPre<D, false>& kp, f32x16& sn0,
                                              f32x16& sn1, const f32x16& sc0, const f32x16& sc1,
                                              const PgenArgs& pa, PgenState& st) {
   constexpr int KK = D / 16;
   constexpr int PD = KK < kQkPD ? KK : kQkPD;
-  const uint8_t* p0 = kbuf + lane * 16;
-  const uint8_t* p1 = p0 + KK * 1024;
+  lds_cptr p1 = p0 + KK * 1024;
   bf16x8 a0[KK], a1[KK];
   if constexpr (QK) {
     if constexpr (PRE) {
@@ -903,8 +920,8 @@ __device__ __forceinline__ PgenOut mma_phase(const uint8_t* kbuf, const bf16x8* 
     }
 #pragma unroll
     for (int kk = PRE ? 1 : 0; kk < PD; ++kk) {
-      a0[kk] = *(const bf16x8*)(p0 + kk * 1024);
-      a1[kk] = *(const bf16x8*)(p1 + kk * 1024);
+      a0[kk] = *(__attribute__((address_space(3))) const bf16x8*)(p0 + kk * 1024);
+      a1[kk] = *(__attribute__((address_space(3))) const bf16x8*)(p1 + kk * 1024);
     }
     sn0 = f32x16{};
     sn1 = f32x16{};
@@ -1071,7 +1088,8 @@ struct PPWave {
   PgenState st;           // block parameters of the tile between V(j) and M(j+1)
   int lane, half, my_q, vis_end;
   int vis_min;            // wave-uniform minimum of vis_end
-  int voff, vsoff;        // lane offsets of the V~ operand reads
+  unsigned klane;         // LDS address of the lane's K operand read in K slot 0
+  unsigned vlane, vslane; // of its V~ code and scale reads in V~ slot 0
   // the pre-read needs registers the bf16 exp-then-quantize variants lack
   static constexpr bool kPreOn = kKPre && (Q8 || EFQ_KPRE_BF16);
   static constexpr int kMPrio = KIND == EFQ_PGEN_EFQ ? EFQ_PRIO_EFQ_M
@@ -1092,19 +1110,20 @@ struct PPWave {
   // Matrix phase M(j): with QK the scores of tile j into sn, and with CODES
   // the codes of tile j-1 (scores sc) in the shadow of those MFMAs, then its
   // P~V and P~1 MFMAs.  PRE: the first K operands are in kp.
+  // kr: byte offset of the K ring slot holding tile j (with QK).
   template <bool QK, bool CODES, bool PRE>
-  __device__ __forceinline__ void mphase(int j, const uint8_t* kbuf0, const VOps<D>& vop,
+  __device__ __forceinline__ void mphase(int j, const uint8_t* kbuf0, int kr, const VOps<D>& vop,
                                          const KPre<D, Q8>& kp, const AttnArgs& a, int b, int hq,
                                          f32x16& sn0, f32x16& sn1, const f32x16& sc0,
                                          const f32x16& sc1) {
     if constexpr (kMPrio != kVPrio) __builtin_amdgcn_s_setprio(kMPrio);
-    const uint8_t* kb = kbuf0 + ((QK ? j : 0) % kPPK) * SmemPP<D, Q8>::kK;
     constexpr bool P = PRE && kPreOn;
     PgenOut po;
     if constexpr (Q8)
-      po = mma_phase8<D, KIND, QK, CODES, P>(kb, qo, kp, lane, sn0, sn1, sc0, sc1, pa, st);
+      po = mma_phase8<D, KIND, QK, CODES, P>(kbuf0 + kr, qo, kp, lane, sn0, sn1, sc0, sc1, pa, st);
     else
-      po = mma_phase<D, KIND, QK, CODES, P>(kb, qo.r, kp, lane, sn0, sn1, sc0, sc1, pa, st);
+      po = mma_phase<D, KIND, QK, CODES, P>(lds_at(klane + kr), qo.r, kp, sn0, sn1, sc0, sc1,
+                                            pa, st);
     if constexpr (CODES) {
       if constexpr (DUMP) {
         const int blk = 2 * (j - 1) + half;
@@ -1134,11 +1153,14 @@ struct PPWave {
   // the block parameters (row maximum, alpha, k_b, bias), and rescale the
   // history when a row maximum moved.  The reads are unconditional so the
   // operands stay in registers.
-  __device__ __forceinline__ void vphase(int j, const uint8_t* vbuf0, const uint8_t* kbuf0,
-                                         f32x16& s0, f32x16& s1, VOps<D>& vop, KPre<D, Q8>& kp) {
+  // vr: byte offset of the V~ ring slot of tile j; krn: of the K slot of
+  // tile j+1.
+  __device__ __forceinline__ void vphase(int j, const uint8_t* vbuf0, int vr, const uint8_t* kbuf0,
+                                         int krn, f32x16& s0, f32x16& s1, VOps<D>& vop,
+                                         KPre<D, Q8>& kp) {
     if constexpr (kMPrio != kVPrio) __builtin_amdgcn_s_setprio(kVPrio);
-    if constexpr (kPreOn) kp.read(kbuf0 + ((j + 1) % kPPK) * SmemPP<D, Q8>::kK, lane);
-    read_v<D>(vbuf0 + (j % kPPV) * SmemPP<D, Q8>::kV, voff, vsoff, vop);
+    if constexpr (kPreOn) kp.read(kbuf0 + krn, lane);
+    read_v<D>(lds_at(vlane + vr), lds_at(vslane + vr), vop);
     // some lane's visible keys end inside this tile
     if ((j + 1) * kBc > vis_min) mask_tile(s0, s1, vis_end - j * kBc, half);
     float pm0, pm1;
@@ -1157,80 +1179,115 @@ struct PPWave {
 // and applies its P~V (j >= 1) and F codes and applies the last tile; group
 // G runs op o in phase o + G.  K(j) is read in phases 2j-1 .. 2j+1 (V(j-1)
 // reads the first operands of M(j) with the K pre-read, else from 2j on)
-// and V~(j) in phases 2j+1, 2j+2.  Even phases t = 2j >= 2 start by
-// streaming tile j+P (K and V~); odd phases end by waiting until only the
-// loads of the last E even phases are outstanding (loads complete in
-// order), E = P-3 with the pre-read, else P-2; phases 4k+3 then end with a
-// workgroup barrier (waves between two barriers are unordered).  A load
-// issued in phase 2j has landed by the end of phase 2(j+P-E)-1, with the
-// pre-read (P = 4, E = 1) 2(j+P)-5, and the next barrier, at the end of
-// phase 2(j+P)-5 or 2(j+P)-3, precedes the pre-read of K(j+P) in phase
-// 2(j+P)-1.  The slots it overwrites (K(j-2) in a ring of P+2, V~(j-3) in a
-// ring of P+3) were last read, and the reads consumed, by phase 2j-3,
-// before a barrier that precedes phase 2j.  Fewer barriers let the groups
-// drift within four phases; each one dropped measured 1-6 % faster than a
-// barrier per phase.  Every wave runs 2 ntiles + 2 phases, so all pass the
-// same barriers.  Scores alternate between two register sets.
+// and V~(j) in phases 2j+1, 2j+2.  Even phases t = 2j >= 2 stream tile j+P
+// (K and V~; past the last tile the last one again, into the slot tile j+P
+// would take, so every wave issues the same loads in every even phase);
+// odd phases end by waiting until only the loads of the last E even phases
+// are outstanding (loads complete in order), E = P-3 with the pre-read,
+// else P-2; phases 4k+3 then end with a workgroup barrier (waves between
+// two barriers are unordered).  A load issued in phase 2j has landed by the
+// end of phase 2(j+P-E)-1, with the pre-read (P = 4, E = 1) 2(j+P)-5, and
+// the next barrier, at the end of phase 2(j+P)-5 or 2(j+P)-3, precedes the
+// pre-read of K(j+P) in phase 2(j+P)-1.  The slots it overwrites (K(j-2) in
+// a ring of P+2, V~(j-3) in a ring of P+3) were last read, and the reads
+// consumed, by phase 2j-3, before a barrier that precedes phase 2j.  Fewer
+// barriers let the groups drift within four phases; each one dropped
+// measured 1-6 % faster than a barrier per phase.  Every wave runs
+// 2 ntiles + 2 phases, so all pass the same barriers.  Scores alternate
+// between two register sets.  The phase index modulo 4 is a compile-time
+// constant in the tile loop, so its phase ends compile to straight-line
+// code; ring slots advance by one tile per phase pair.
+template <int X>
+using IC = std::integral_constant<int, X>;
+
+template <int STEP, int DEPTH>
+__device__ __forceinline__ int ring_next(int off) {
+  off += STEP;
+  return off == STEP * DEPTH ? 0 : off;
+}
+
 template <int G, int D, int KIND, bool DUMP, bool Q8, typename Stream>
 __device__ __forceinline__ void pp_schedule(PPWave<D, KIND, DUMP, Q8>& w, int T, int ntiles,
                                             const uint8_t* kbuf0, const uint8_t* vbuf0,
-                                            const AttnArgs& a, int b, int hq,
-                                            int per_tile, Stream stream) {
+                                            const AttnArgs& a, int b, int hq, int keep,
+                                            Stream& stream) {
+  using Sm = SmemPP<D, Q8>;
   f32x16 sa0, sa1, sb0, sb1;
   VOps<D> vop;
   KPre<D, Q8> kp;      // first K operands of the next matrix phase
-  int t = 0;   // phase
+  int kr = 0;          // K slot of the next matrix phase with Q K^T
+  int vr = 0;          // V~ slot of the next VALU phase
+  auto knext = [](int x) { return ring_next<Sm::kK, kPPK>(x); };
+  auto vnext = [](int x) { return ring_next<Sm::kV, kPPV>(x); };
   // bf16 Q K^T: the tile loads go out after the even phase's work, not
   // before it (measured 1.5 % faster; the MXFP8 path is faster with them
   // first).  Either way they belong to phase t, as the schedule assumes.
   constexpr bool kLate = !Q8;
-  auto begin = [&]() {
-    if constexpr (!kLate)
-      if ((t & 1) == 0 && t >= 2) stream(t >> 1);
+  // Phase t with TM = t % 4 known (even TM only for t >= 2); TM = 4 is t = 0.
+  auto begin = [&](auto tm) {
+    constexpr int TM = decltype(tm)::value;
+    if constexpr (!kLate && (TM == 0 || TM == 2)) stream();
   };
-  auto end = [&]() {
-    if constexpr (kLate) {
-      if ((t & 1) == 0 && t >= 2) {
-        __builtin_amdgcn_sched_barrier(0);
-        stream(t >> 1);
-      }
+  auto end = [&](auto tm) {
+    constexpr int TM = decltype(tm)::value;
+    if constexpr (kLate && (TM == 0 || TM == 2)) {
+      __builtin_amdgcn_sched_barrier(0);
+      stream();
     }
-    if (t & 1) {
-      // the batches of the last kKeep even phases 2(k-i) (tiles k-i+P; the
-      // prologue stands in for phases <= 0) may stay in flight: per_tile
-      // loads each, none for a tile past the end
-      const int k = t >> 1;
-      int n = 0;
-#pragma unroll
-      for (int i = 0; i < kKeep; ++i) n += k - i + kPP < ntiles ? per_tile : 0;
-      wait_vmem_le(n);
-      if ((t & (kBarPhases - 1)) == kBarPhases - 1) wg_barrier();
+    if constexpr (TM == 1 || TM == 3) {
+      // the batches of the last kKeep even phases may stay in flight
+      wait_vmem_le(keep);
+      if constexpr (TM == 3) wg_barrier();
       else __builtin_amdgcn_sched_barrier(0);
     } else {
       __builtin_amdgcn_sched_barrier(0);
     }
-    ++t;
   };
-  if (G == 1) { begin(); end(); }
-  // M(0), V(0); every later M(j) with Q K^T follows a V(j-1) that pre-read
-  // its first K operands (j < T)
-  begin(); w.template mphase<true, false, false>(0, kbuf0, vop, kp, a, b, hq, sa0, sa1, sb0, sb1); end();
-  begin(); w.vphase(0, vbuf0, kbuf0, sa0, sa1, vop, kp); end();
+  constexpr int TA = (2 + G) & 3, TB = (3 + G) & 3, TC = G, TD = (1 + G) & 3;
+  // M(0), V(0) (group 1 after an empty phase); every later M(j) with Q K^T
+  // follows a V(j-1) that pre-read its first K operands (j < T)
+  if constexpr (G == 0) {
+    begin(IC<4>{}); w.template mphase<true, false, false>(0, kbuf0, kr, vop, kp, a, b, hq, sa0, sa1, sb0, sb1); end(IC<4>{});
+    kr = knext(kr);
+    begin(IC<1>{}); w.vphase(0, vbuf0, vr, kbuf0, kr, sa0, sa1, vop, kp); end(IC<1>{});
+  } else {
+    begin(IC<4>{}); end(IC<4>{});
+    begin(IC<1>{}); w.template mphase<true, false, false>(0, kbuf0, kr, vop, kp, a, b, hq, sa0, sa1, sb0, sb1); end(IC<1>{});
+    kr = knext(kr);
+    begin(IC<2>{}); w.vphase(0, vbuf0, vr, kbuf0, kr, sa0, sa1, vop, kp); end(IC<2>{});
+  }
+  vr = vnext(vr);
   int j = 1;
   for (; j + 1 < T; j += 2) {
-    begin(); w.template mphase<true, true, true>(j, kbuf0, vop, kp, a, b, hq, sb0, sb1, sa0, sa1); end();
-    begin(); w.vphase(j, vbuf0, kbuf0, sb0, sb1, vop, kp); end();
-    begin(); w.template mphase<true, true, true>(j + 1, kbuf0, vop, kp, a, b, hq, sa0, sa1, sb0, sb1); end();
-    begin(); w.vphase(j + 1, vbuf0, kbuf0, sa0, sa1, vop, kp); end();
+    begin(IC<TA>{}); w.template mphase<true, true, true>(j, kbuf0, kr, vop, kp, a, b, hq, sb0, sb1, sa0, sa1); end(IC<TA>{});
+    kr = knext(kr);
+    begin(IC<TB>{}); w.vphase(j, vbuf0, vr, kbuf0, kr, sb0, sb1, vop, kp); end(IC<TB>{});
+    vr = vnext(vr);
+    begin(IC<TC>{}); w.template mphase<true, true, true>(j + 1, kbuf0, kr, vop, kp, a, b, hq, sa0, sa1, sb0, sb1); end(IC<TC>{});
+    kr = knext(kr);
+    begin(IC<TD>{}); w.vphase(j + 1, vbuf0, vr, kbuf0, kr, sa0, sa1, vop, kp); end(IC<TD>{});
+    vr = vnext(vr);
   }
   if (j < T) {   // one more tile: its scores go to set b, the last coded from b
-    begin(); w.template mphase<true, true, true>(j, kbuf0, vop, kp, a, b, hq, sb0, sb1, sa0, sa1); end();
-    begin(); w.vphase(j, vbuf0, kbuf0, sb0, sb1, vop, kp); end();
-    begin(); w.template mphase<false, true, false>(T, kbuf0, vop, kp, a, b, hq, sa0, sa1, sb0, sb1); end();
+    begin(IC<TA>{}); w.template mphase<true, true, true>(j, kbuf0, kr, vop, kp, a, b, hq, sb0, sb1, sa0, sa1); end(IC<TA>{});
+    kr = knext(kr);
+    begin(IC<TB>{}); w.vphase(j, vbuf0, vr, kbuf0, kr, sb0, sb1, vop, kp); end(IC<TB>{});
+    begin(IC<TC>{}); w.template mphase<false, true, false>(T, kbuf0, kr, vop, kp, a, b, hq, sa0, sa1, sb0, sb1); end(IC<TC>{});
   } else {       // the last tile's scores are in set a
-    begin(); w.template mphase<false, true, false>(T, kbuf0, vop, kp, a, b, hq, sb0, sb1, sa0, sa1); end();
+    begin(IC<TA>{}); w.template mphase<false, true, false>(T, kbuf0, kr, vop, kp, a, b, hq, sb0, sb1, sa0, sa1); end(IC<TA>{});
   }
-  while (t < 2 * ntiles + 2) { begin(); end(); }
+  // empty phases until the workgroup's last tile (the phase index is known
+  // only at run time here)
+  for (int t = 2 * T + 1 + G; t < 2 * ntiles + 2; ++t) {
+    if ((t & 1) == 0) {
+      stream();
+      __builtin_amdgcn_sched_barrier(0);
+    } else {
+      wait_vmem_le(keep);
+      if ((t & 3) == 3) wg_barrier();
+      else __builtin_amdgcn_sched_barrier(0);
+    }
+  }
 }
 
 // Q8: q and k are the MXFP8 buffers Q^ and K^ (E4M3 codes, then E8M0 scales
@@ -1287,29 +1344,27 @@ attn_pp_kernel(const void* __restrict__ q, const void* __restrict__ k,
   w.vis_end = CAUSAL ? min(a.Sk, w.my_q + 1) : a.Sk;
   // lane 0 holds the wave's first query, whose visible range is the shortest
   w.vis_min = __builtin_amdgcn_readfirstlane(CAUSAL ? min(a.Sk, q_wave0 + 1) : a.Sk);
-  // the lane offsets stay in registers across the loop instead of being
-  // recomputed from the lane index in every phase
-  w.voff = vop_offset<D>(w.lane);
-  w.vsoff = vscale_offset<D>(w.lane);
-  asm volatile("" : "+v"(w.voff), "+v"(w.vsoff));
+  uint8_t* const kbuf0 = smem + Sm::kKOff;
+  uint8_t* const vbuf0 = smem + Sm::kVOff;
+  // the lane's LDS read addresses in ring slot 0 stay in registers across
+  // the loop instead of being recomputed from the lane index in every phase
+  w.klane = lds_addr(kbuf0 + w.lane * 16);
+  w.vlane = lds_addr(vbuf0 + vop_offset<D>(w.lane));
+  w.vslane = lds_addr(vbuf0 + vscale_offset<D>(w.lane));
+  asm volatile("" : "+v"(w.klane), "+v"(w.vlane), "+v"(w.vslane));
 
   std::conditional_t<Q8, KLoad8<D, kPPWaves>, KLoad<D, kPPWaves>> kload;
-  int k_issued;
   if constexpr (Q8) {
     const uint8_t* kh = (const uint8_t*)k;
     const long hrow = ((long)b * a.Hkv + g) * a.sk_pad;
     kload.init(kh + hrow * D, kh + a.k8_soff + hrow * (D / 32), a.sk_pad, wave, w.lane);
-    k_issued = KLoad8<D, kPPWaves>::issued(wave);
   } else {
     kload.init((const unsigned short*)k + (long)b * a.Sk * a.Hkv * D, a.Sk, a.Hkv, g, wave, w.lane);
-    k_issued = KLoad<D, kPPWaves>::kIssued;
   }
-  VLoad<D, kPPWaves> vload;
+  using VL = VLoad<D, kPPWaves>;
+  VL vload;
   vload.init(vhat + ((long)b * a.Hkv + g) * a.nb * D * 16,
-             vhat + a.scale_off + ((long)b * a.Hkv + g) * a.nb * D, a.nb);
-  uint8_t* const kbuf0 = smem + Sm::kKOff;
-  uint8_t* const vbuf0 = smem + Sm::kVOff;
-  const int v_issued = VLoad<D, kPPWaves>::issued(wave);
+             vhat + a.scale_off + ((long)b * a.Hkv + g) * a.nb * D, a.nb, w.lane);
 
   w.pa.scale = a.scale;
   w.pa.sh = a.scale * a.h;
@@ -1324,32 +1379,55 @@ attn_pp_kernel(const void* __restrict__ q, const void* __restrict__ k,
   w.sel = rowsum_selector(w.lane);
   w.m = -INFINITY;
 
-  // Streams tile x (K into ring slot x % (P+2), V~ into x % (P+3)) if it
-  // exists; returns the number of loads issued.
-  auto load_tile = [&](int x) {
-    if (x >= ntiles) return 0;
-    if constexpr (Q8) kload.issue(kbuf0 + (x % kPPK) * Sm::kK, x, wave, w.lane);
-    else kload.issue(kbuf0 + (x % kPPK) * Sm::kK, x, wave);
-    vload.issue(vbuf0 + (x % kPPV) * Sm::kV, x, wave, w.lane);
-    return k_issued + v_issued;
+  // Streams tile x into the ring slots at byte offsets kofs, vofs: K (or
+  // K^ codes and scales) and V~ codes and scales.  Every wave issues kLoads
+  // loads: its K blocks and one V~ code block, or, where a wave has fewer,
+  // a copy of a scale load (several waves write the same bytes to the same
+  // place).  Past the last tile (x >= ntiles) the last tile is loaded
+  // again, so the count never changes and the waits are constants.
+  constexpr int kLoads = Q8 ? 2 : KLoad<D, kPPWaves>::kIssued + 1;
+  auto load_tile = [&](int x, int kofs, int vofs) {
+    const int xt = x < ntiles ? x : ntiles - 1;
+    uint8_t* const kb = kbuf0 + kofs;
+    uint8_t* const vb = vbuf0 + vofs;
+    if constexpr (Q8) {
+      using K8 = KLoad8<D, kPPWaves>;
+      // waves with a K^ code block: that and a V~ code block or a scale
+      // load; the others (D = 64) two scale loads
+      if (wave < K8::NBLK) kload.issue_codes(kb, xt, wave);
+      else if (wave & 1) vload.issue_scales(vb, xt);
+      else kload.issue_scales(kb, xt, w.lane);
+      if (wave < VL::NB) vload.issue_codes(vb, xt, wave, w.lane);
+      else if (wave & 1) kload.issue_scales(kb, xt, w.lane);
+      else vload.issue_scales(vb, xt);
+    } else {
+      kload.issue(kb, xt, wave);
+      if (wave < VL::NB) vload.issue_codes(vb, xt, wave, w.lane);
+      else vload.issue_scales(vb, xt);
+    }
   };
   // prologue: tiles 0 .. P; tiles 0 and 1 resident, 2 .. P in flight (the
   // loads of the last P-1 even phases before phase 2)
-  load_tile(0);
-  load_tile(1);
-  int pending = 0;
 #pragma unroll
-  for (int x = 2; x <= kPP; ++x) pending += load_tile(x);
-  wait_vmem_le(pending);
+  for (int x = 0; x <= kPP; ++x) load_tile(x, (x % kPPK) * Sm::kK, (x % kPPV) * Sm::kV);
+  wait_vmem_le((kPP - 1) * kLoads);
   __syncthreads();
 
-  // phase 2j (j >= 1) streams tile j+P
-  auto stream = [&](int j) { return load_tile(j + kPP); };
+  // phase 2j (j >= 1) streams tile j+P; the slots advance with the tile
+  int sx = kPP + 1;
+  int skofs = ((kPP + 1) % kPPK) * Sm::kK, svofs = ((kPP + 1) % kPPV) * Sm::kV;
+  auto stream = [&]() {
+    load_tile(sx, skofs, svofs);
+    ++sx;
+    skofs = ring_next<Sm::kK, kPPK>(skofs);
+    svofs = ring_next<Sm::kV, kPPV>(svofs);
+  };
 
+  constexpr int keep = kKeep * kLoads;
   if (group == 0)
-    pp_schedule<0>(w, wtiles, ntiles, kbuf0, vbuf0, a, b, hq, k_issued + v_issued, stream);
+    pp_schedule<0>(w, wtiles, ntiles, kbuf0, vbuf0, a, b, hq, keep, stream);
   else
-    pp_schedule<1>(w, wtiles, ntiles, kbuf0, vbuf0, a, b, hq, k_issued + v_issued, stream);
+    pp_schedule<1>(w, wtiles, ntiles, kbuf0, vbuf0, a, b, hq, keep, stream);
   wait_vmem();   // no load may still target LDS when the wave leaves
 
   // O = A / l as A * (1 / l): one division per row instead of one per

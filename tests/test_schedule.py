@@ -35,13 +35,26 @@ def test_constants_match_kernel_source():
     assert "constexpr int kPPV = kPP + 3;" in src
     assert "constexpr int kBarPhases = 4;" in src
     assert "constexpr int kKeep = kPP - 2 - (kKPre ? 1 : 0);" in src
-    # the barrier sits in the odd-phase branch of the phase end, once every
-    # kBarPhases phases
-    end = src[src.index("auto end = [&]() {"):]
-    end = end[:end.index("};")]
-    odd = end[end.index("if (t & 1) {"):end.index("} else {\n      __builtin_amdgcn_sched_barrier(0);\n    }\n    ++t;")]
-    assert "if ((t & (kBarPhases - 1)) == kBarPhases - 1) wg_barrier();" in odd
+    # every wave issues the same loads in every even phase (past the last
+    # tile, the last tile again), so the landing wait is one constant
+    assert "constexpr int keep = kKeep * kLoads;" in src
+    assert "const int xt = x < ntiles ? x : ntiles - 1;" in src
+    # the phase end with t % 4 known at compile time: wait at odd phases,
+    # the barrier at phase 3 (mod 4) only
+    end = src[src.index("  auto end = [&](auto tm) {"):]
+    end = end[:end.index("\n  };")]
+    assert "if constexpr (TM == 1 || TM == 3) {" in end
+    assert "wait_vmem_le(keep);" in end
+    assert "if constexpr (TM == 3) wg_barrier();" in end
     assert end.count("wg_barrier") == 1
+    # the loop's phases: M(j), V(j), M(j+1), V(j+1) of group G at t = 2j + G
+    # (j odd) .. 2j + 3 + G
+    assert "constexpr int TA = (2 + G) & 3, TB = (3 + G) & 3, TC = G, TD = (1 + G) & 3;" in src
+    # the empty phases after the wave's last tile, with t at run time
+    tail = src[src.index("  for (int t = 2 * T + 1 + G; t < 2 * ntiles + 2; ++t) {"):]
+    tail = tail[:tail.index("\n  }\n")]
+    assert "wait_vmem_le(keep);" in tail
+    assert "if ((t & 3) == 3) wg_barrier();" in tail
 
 
 def landing_phase(x):
@@ -83,8 +96,10 @@ def test_ring_schedule_is_safe(pre):
             assert x < ntiles
             assert interval(landing_phase(x)) < interval(t) or landing_phase(x) < 0, (kind, x, t)
             cases += 1
-        # every refill comes after the consumption of the slot's previous tile
-        for x in range(P + 1, ntiles):
+        # every refill comes after the consumption of the slot's previous
+        # tile; the even phases 2 .. 2 ntiles stream tiles P+1 .. ntiles+P,
+        # those past the end as copies of the last tile into their own slots
+        for x in range(P + 1, ntiles + P + 1):
             issue = 2 * (x - P)
             for kind, ring in (("K", KRING), ("V", VRING)):
                 old = x - ring
