@@ -180,9 +180,13 @@ def counters(dirs, out: str, workload: str, command: str):
         fh.write("# wait / wait-issue: wave cycles waiting on a dependency or counter "
                  "(SQ_WAIT_ANY) and with an instruction ready but not issued "
                  "(SQ_WAIT_INST_ANY), per SIMD cycle, summed over the SIMD's waves\n")
+        fh.write("# LDS busy: SQ_LDS_IDX_ACTIVE per CU cycle (4 per 1 KB ds_read_b128, i.e. "
+                 "cycles at 256 B/clk); TA coalesced: TA_BUFFER_COALESCED_READ_CYCLES / "
+                 "TA_BUFFER_TOTAL_CYCLES; TA busy: TA_BUFFER_TOTAL_CYCLES per TA cycle\n")
         fh.write("# kernel | cycles | MFMA busy | VALU active | co-exec | wait | wait-issue | "
                  "VALU instr per SIMD | MFMA instr per SIMD | SALU instr per SIMD | "
-                 "VALU per score | LDS instr per SIMD | bank-conflict cycles per LDS instr\n")
+                 "VALU per score | LDS instr per SIMD | bank-conflict cycles per LDS instr | "
+                 "LDS busy | TA coalesced | TA busy\n")
         per_kind = {}
         for key in sorted(acc):
             c = acc[key]
@@ -197,7 +201,10 @@ def counters(dirs, out: str, workload: str, command: str):
                      f"{c.get('SQ_INSTS_SALU', float('nan')) / simds:.0f} | "
                      f"{c.get('SQ_INSTS_VALU', float('nan')) * 64 / pairs:.2f} | "
                      f"{c.get('SQ_INSTS_LDS', float('nan')) / simds:.0f} | "
-                     f"{c.get('SQ_LDS_BANK_CONFLICT', 0) / max(c.get('SQ_INSTS_LDS', 0), 1):.4f}\n")
+                     f"{c.get('SQ_LDS_BANK_CONFLICT', 0) / max(c.get('SQ_INSTS_LDS', 0), 1):.4f} | "
+                     f"{c.get('SQ_LDS_IDX_ACTIVE', float('nan')) / (simds / 4) / cyc:.3f} | "
+                     f"{c.get('TA_BUFFER_COALESCED_READ_CYCLES', float('nan')) / max(c.get('TA_BUFFER_TOTAL_CYCLES', 0), 1):.3f} | "
+                     f"{c.get('TA_BUFFER_TOTAL_CYCLES', float('nan')) / (simds / 4) / cyc:.3f}\n")
             if names[key] in kinds:
                 per_kind[kinds[names[key]]] = (va, g("SQ_VALU_MFMA_BUSY_CYCLES"))
         for kind, (va, mf) in sorted(per_kind.items()):
@@ -221,9 +228,15 @@ def main():
         return
     import bench
     from paper_2609_09721_amd import inputs
-    fetch_dir, write_dir, wl = sys.argv[2], sys.argv[3], sys.argv[4]
-    out = sys.argv[5] if len(sys.argv) > 5 else os.path.join(ROOT, "profiles",
-                                                             f"attn_fwd_{wl}_traffic.txt")
+    args = sys.argv[2:]
+    l2_dir = None
+    if "--l2" in args:
+        i = args.index("--l2")
+        l2_dir = args[i + 1]
+        del args[i:i + 2]
+    fetch_dir, write_dir, wl = args[0], args[1], args[2]
+    out = args[3] if len(args) > 3 else os.path.join(ROOT, "profiles",
+                                                     f"attn_fwd_{wl}_traffic.txt")
     is_attn = lambda n: "attn_pp_kernel" in n or "attn_fwd_kernel" in n
     is_copy = lambda n: "copyBuffer" in n
     f = per_dispatch(fetch_dir, "FETCH_SIZE")
@@ -240,6 +253,7 @@ def main():
             + w.batch * w.seq * w.heads_kv * w.head_dim * 2            # K bf16
             + w.batch * w.heads_kv * 2 * ((w.seq + 63) // 64) * w.head_dim * 17  # V~
             + w.batch * w.seq * w.heads_q * w.head_dim * 4)            # O fp32
+    algo_rd = algo - w.batch * w.seq * w.heads_q * w.head_dim * 4
     with open(out, "w") as fh:
         fh.write(f"# HBM traffic of one attention launch, {wl} (EFQ), from rocprofv3 counters\n")
         fh.write("# commands (from the repository root, TMPDIR=/tmp):\n")
@@ -247,7 +261,11 @@ def main():
                  f"python3 bench.py --pmc-run --workload {wl}\n")
         fh.write("#   rocprofv3 --pmc WRITE_SIZE -d <WRITE_DIR> -o p --output-format csv -- "
                  f"python3 bench.py --pmc-run --workload {wl}\n")
-        fh.write(f"#   python3 -m paper_2609_09721_amd.profsum traffic <FETCH_DIR> <WRITE_DIR> {wl}\n")
+        if l2_dir:
+            fh.write("#   rocprofv3 --pmc TCC_HIT_sum TCC_MISS_sum TCC_EA0_RDREQ_sum TCC_EA0_RDREQ_DRAM_sum "
+                     f"-d <L2_DIR> -o p --output-format csv -- python3 bench.py --pmc-run --workload {wl}\n")
+        fh.write(f"#   python3 -m paper_2609_09721_amd.profsum traffic <FETCH_DIR> <WRITE_DIR> {wl}"
+                 + (" --l2 <L2_DIR>" if l2_dir else "") + "\n")
         fh.write(f"# attention dispatches {na}, copy dispatches {nc}; copy size {bench.COPY_BYTES} B\n")
         fh.write(f"fetch_counter_attn = {fa:.1f}\nfetch_counter_copy = {fc:.1f}\n")
         fh.write(f"write_counter_attn = {wa:.1f}\nwrite_counter_copy = {wc:.1f}\n")
@@ -255,6 +273,16 @@ def main():
         fh.write(f"read_bytes_per_launch = {rd:.0f}\nwrite_bytes_per_launch = {wb:.0f}\n")
         fh.write(f"algorithmic_bytes_per_launch = {algo}\n")
         fh.write(f"traffic_bytes_per_launch = {rd + wb:.0f}\n")
+        fh.write(f"algorithmic_read_bytes_per_launch = {algo_rd}\n")
+        fh.write(f"read_over_algorithmic = {rd / algo_rd:.3f}\n")
+        if l2_dir:
+            hit, _ = mean_of(per_dispatch(l2_dir, "TCC_HIT_sum"), is_attn)
+            miss, _ = mean_of(per_dispatch(l2_dir, "TCC_MISS_sum"), is_attn)
+            ea, _ = mean_of(per_dispatch(l2_dir, "TCC_EA0_RDREQ_sum"), is_attn)
+            dram, _ = mean_of(per_dispatch(l2_dir, "TCC_EA0_RDREQ_DRAM_sum"), is_attn)
+            fh.write(f"l2_hit_rate = {hit / max(hit + miss, 1):.4f}\n")
+            fh.write(f"l2_read_requests_to_memory = {ea:.0f}\n")
+            fh.write(f"of_them_to_dram = {dram:.0f}\n")
         fh.write(f"kernel_hash = {bench.kernel_hash()}\n")
     print(open(out).read())
 
