@@ -88,9 +88,9 @@ __device__ __forceinline__ void swap32f(float& a, float& b) {
   b = __uint_as_float(ub);
 }
 
-// Maximum of two values that came through an integer lane swap: an IEEE
-// maximum would first quiet each operand (two more instructions); scores
-// are never NaN, so the plain instruction is exact.
+// Maximum of two values that came through an integer lane swap or are
+// themselves maxima: an IEEE maximum would first quiet each operand (more
+// instructions); scores are never NaN, so the plain instruction is exact.
 __device__ __forceinline__ float fmax_swapped(float a, float b) {
   float r;
   asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
@@ -200,7 +200,8 @@ __device__ __forceinline__ void pg_params(float pm0, float pm1, float& m, const 
     float t0 = bmine, t1 = bmine;
     swap32f(t0, t1);                            // (block 0 max, block 1 max) in every lane
     const float mt = fmax_swapped(t0, t1) * unit;   // rowmax S^j (monotone in the raw max)
-    const float mnew = __builtin_fmaxf(m, mt);
+    // m is itself a maximum (or -inf), so no operand quieting is needed
+    const float mnew = fmax_swapped(m, mt);
     // alpha = exp(m^{j-1} - m^j), Eq. (alpha); exactly 1 when the max is unchanged
     const float d = LOG2 ? (m - mnew) : (m - mnew) * kInvLn2;
     st.alpha = (m == mnew) ? 1.0f : __builtin_amdgcn_exp2f(d);
@@ -780,8 +781,9 @@ __device__ __forceinline__ void pv_slabs(f32x16* oacc, const VOps<D>& v, const i
 // Mask keys past the end and, for causal attention, keys after the query
 // (the mask acts before the probability stage).  lim = number of visible
 // keys of this lane counted from the tile start.
-__device__ __forceinline__ void mask_tile(f32x16& s0, f32x16& s1, int lim, int half) {
-  const int l0 = lim - 4 * half;   // the per-register key offsets stay immediates
+__device__ __forceinline__ void mask_tile(f32x16& s0, f32x16& s1, int l0) {
+  // l0 = visible keys counted from the tile start, less 4 half: the
+  // per-register key offsets stay immediates
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int kofs = 8 * (r >> 2) + (r & 3);
@@ -1086,8 +1088,9 @@ struct PPWave {
   float m;
   PgenArgs pa;
   PgenState st;           // block parameters of the tile between V(j) and M(j+1)
-  int lane, half, my_q, vis_end;
-  int vis_min;            // wave-uniform minimum of vis_end
+  int lane, half, my_q;
+  int vis_end4;           // visible keys of the lane's query, less 4 half
+  int vis_min;            // wave-uniform minimum of the visible key counts
   unsigned klane;         // LDS address of the lane's K operand read in K slot 0
   unsigned vlane, vslane; // of its V~ code and scale reads in V~ slot 0
   // the pre-read needs registers the bf16 exp-then-quantize variants lack
@@ -1162,7 +1165,8 @@ struct PPWave {
     if constexpr (kPreOn) kp.read(kbuf0 + krn, lane);
     read_v<D>(lds_at(vlane + vr), lds_at(vslane + vr), vop);
     // some lane's visible keys end inside this tile
-    if ((j + 1) * kBc > vis_min) mask_tile(s0, s1, vis_end - j * kBc, half);
+    if ((j + 1) * kBc > __builtin_amdgcn_readfirstlane(vis_min))
+      mask_tile(s0, s1, vis_end4 - j * kBc);
     float pm0, pm1;
     pg_max<KIND>(s0, s1, pm0, pm1);
     pg_params<KIND>(pm0, pm1, m, pa, st);
@@ -1341,7 +1345,7 @@ attn_pp_kernel(const void* __restrict__ q, const void* __restrict__ k,
   const int wave_end = CAUSAL ? min(a.Sk, q_wave0 + kWaveQ) : a.Sk;
   const int ntiles = (kv_end + kBc - 1) / kBc;
   const int wtiles = (wave_end + kBc - 1) / kBc;
-  w.vis_end = CAUSAL ? min(a.Sk, w.my_q + 1) : a.Sk;
+  w.vis_end4 = (CAUSAL ? min(a.Sk, w.my_q + 1) : a.Sk) - 4 * w.half;
   // lane 0 holds the wave's first query, whose visible range is the shortest
   w.vis_min = __builtin_amdgcn_readfirstlane(CAUSAL ? min(a.Sk, q_wave0 + 1) : a.Sk);
   uint8_t* const kbuf0 = smem + Sm::kKOff;
