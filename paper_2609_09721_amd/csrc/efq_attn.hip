@@ -184,14 +184,16 @@ __device__ __forceinline__ void pg_max(const f32x16& s0, const f32x16& s1, float
 template <int KIND>
 constexpr bool is_expq() { return KIND == EFQ_PGEN_EXPQ || KIND == EFQ_PGEN_EXPQ6; }
 
+// Returns whether some row maximum of the wave moved (wave-uniform).
 template <int KIND>
-__device__ __forceinline__ void pg_params(float pm0, float pm1, float& m, const PgenArgs& pa,
+__device__ __forceinline__ bool pg_params(float pm0, float pm1, float& m, const PgenArgs& pa,
                                           PgenState& st) {
+  bool moved = false;
   if constexpr (KIND == EFQ_PGEN_NOOP) {
     st.scale_b = 127 - 6;
     st.alpha = 1.0f;
     st.w[0] = st.w[1] = st.w[2] = st.w[3] = 0x22222222u;
-    return;
+    return moved;
   } else {
     constexpr bool LOG2 = is_expq<KIND>();
     const float unit = LOG2 ? pa.l2s : pa.scale;
@@ -205,6 +207,7 @@ __device__ __forceinline__ void pg_params(float pm0, float pm1, float& m, const 
     // alpha = exp(m^{j-1} - m^j), Eq. (alpha); exactly 1 when the max is unchanged
     const float d = LOG2 ? (m - mnew) : (m - mnew) * kInvLn2;
     st.alpha = (m == mnew) ? 1.0f : __builtin_amdgcn_exp2f(d);
+    moved = __builtin_amdgcn_ballot_w64(m != mnew) != 0ull;
     m = mnew;
     if constexpr (is_expq<KIND>()) {
       // exp-then-quantize, Eq. (post-softmax-path): max_t exp(x_t) =
@@ -246,6 +249,7 @@ __device__ __forceinline__ void pg_params(float pm0, float pm1, float& m, const 
       st.scale_b = kb + 127;
     }
   }
+  return moved;
 }
 
 // EFQ-Softmax-LUT, Sec. II-D: the 16-level index j16 = clip(floor(u) + 1,
@@ -608,19 +612,21 @@ struct VLoad {
   const uint8_t* codes;
   const uint8_t* scales;
   int nb;
+  int coff_lane;                                         // lane's byte offset of the code load
   int soff_lane;                                         // lane's byte offset of the scale load
   __device__ void init(const uint8_t* vcodes, const uint8_t* vscales, int nblocks, int lane) {
     codes = vcodes;
     scales = vscales;
     nb = nblocks;
+    coff_lane = lane * 16;
     // 2 D scale bytes as dwords; for D = 64 the upper lanes repeat the
     // lower ones into the padding
     soff_lane = (lane % (2 * D / 4)) * 4;
   }
   // code block `wave` (waves below NB)
-  __device__ void issue_codes(uint8_t* vbuf, int tile, int wave, int lane) const {
+  __device__ void issue_codes(uint8_t* vbuf, int tile, int wave) const {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(make_rsrc(codes, (unsigned)(nb * D * 16)),
-                                             vbuf + wave * 1024, 16, lane * 16,
+                                             vbuf + wave * 1024, 16, coff_lane,
                                              tile * 2 * D * 16 + wave * 1024, 0, 0);
   }
   // the tile's scales; several waves may load them (same bytes, same place)
@@ -1169,8 +1175,7 @@ struct PPWave {
       mask_tile(s0, s1, vis_end4 - j * kBc);
     float pm0, pm1;
     pg_max<KIND>(s0, s1, pm0, pm1);
-    pg_params<KIND>(pm0, pm1, m, pa, st);
-    if (__builtin_amdgcn_ballot_w64(st.alpha != 1.0f) != 0ull) {
+    if (pg_params<KIND>(pm0, pm1, m, pa, st)) {
 #pragma unroll
       for (int s = 0; s < NS; ++s) oacc[s] *= st.alpha;
       lacc[0] *= st.alpha;
@@ -1369,6 +1374,7 @@ attn_pp_kernel(const void* __restrict__ q, const void* __restrict__ k,
   VL vload;
   vload.init(vhat + ((long)b * a.Hkv + g) * a.nb * D * 16,
              vhat + a.scale_off + ((long)b * a.Hkv + g) * a.nb * D, a.nb, w.lane);
+  asm volatile("" : "+v"(vload.coff_lane), "+v"(vload.soff_lane));
 
   w.pa.scale = a.scale;
   w.pa.sh = a.scale * a.h;
@@ -1401,12 +1407,12 @@ attn_pp_kernel(const void* __restrict__ q, const void* __restrict__ k,
       if (wave < K8::NBLK) kload.issue_codes(kb, xt, wave);
       else if (wave & 1) vload.issue_scales(vb, xt);
       else kload.issue_scales(kb, xt, w.lane);
-      if (wave < VL::NB) vload.issue_codes(vb, xt, wave, w.lane);
+      if (wave < VL::NB) vload.issue_codes(vb, xt, wave);
       else if (wave & 1) kload.issue_scales(kb, xt, w.lane);
       else vload.issue_scales(vb, xt);
     } else {
       kload.issue(kb, xt, wave);
-      if (wave < VL::NB) vload.issue_codes(vb, xt, wave, w.lane);
+      if (wave < VL::NB) vload.issue_codes(vb, xt, wave);
       else vload.issue_scales(vb, xt);
     }
   };
