@@ -903,6 +903,18 @@ __device__ __forceinline__ void mc_regions(lds_cptr p0, lds_cptr p1, bf16x8* a0,
     }
     constexpr int P0 = 16 * I / KK, P1 = 16 * (I + 1) / KK;
     pg_pairs<KIND, 2 * P0, 2 * P1>(sc0, sc1, pa, st);
+    if constexpr (QK && KIND == EFQ_PGEN_EFQ) {
+      // EFQ: each MFMA, then one LDS operand read, then about half of the
+      // region's code-step instructions (measured 1 % faster than the
+      // compiler's own placement, which bunches them after the first MFMA;
+      // the LUT and exp-then-quantize stages were 4-7 % slower with it)
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
+      __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);   // VALU
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 7, 0);
+    }
     __builtin_amdgcn_sched_barrier(0);
     mc_regions<D, KIND, QK, I + 1>(p0, p1, a0, a1, qreg, sn0, sn1, sc0, sc1, pa, st);
   }
