@@ -199,14 +199,19 @@ __device__ __forceinline__ bool pg_params(float pm0, float pm1, float& m, const 
     const float unit = LOG2 ? pa.l2s : pa.scale;
     swap32f(pm0, pm1);                          // lower: (own, partner) block 0; upper: block 1
     const float bmine = fmax_swapped(pm0, pm1);  // raw maximum of the lane's own block
-    float t0 = bmine, t1 = bmine;
+    // the lane's block maximum in score units; rounding is monotone, so the
+    // row maximum of the products is the product of the raw row maximum
+    const float bs = bmine * unit;
+    float t0 = bs, t1 = bs;
     swap32f(t0, t1);                            // (block 0 max, block 1 max) in every lane
-    const float mt = fmax_swapped(t0, t1) * unit;   // rowmax S^j (monotone in the raw max)
+    const float mt = fmax_swapped(t0, t1);      // rowmax S^j
     // m is itself a maximum (or -inf), so no operand quieting is needed
     const float mnew = fmax_swapped(m, mt);
-    // alpha = exp(m^{j-1} - m^j), Eq. (alpha); exactly 1 when the max is unchanged
+    // alpha = exp(m^{j-1} - m^j), Eq. (alpha): exp2(0) = 1 exactly when the
+    // max is unchanged, exp2(-inf) = 0 on the first tile; m^j is finite from
+    // the first tile on (key 0 is visible to every query), so d is never NaN
     const float d = LOG2 ? (m - mnew) : (m - mnew) * kInvLn2;
-    st.alpha = (m == mnew) ? 1.0f : __builtin_amdgcn_exp2f(d);
+    st.alpha = __builtin_amdgcn_exp2f(d);
     moved = __builtin_amdgcn_ballot_w64(m != mnew) != 0ull;
     m = mnew;
     if constexpr (is_expq<KIND>()) {
@@ -214,7 +219,7 @@ __device__ __forceinline__ bool pg_params(float pm0, float pm1, float& m, const 
       // exp(max_t x_t); the shift S2 - m2 is exact at the row maximum, so it
       // gets p = 1 exactly (an fma of the unshifted score could land on the
       // wrong side of the power-of-two scale boundary)
-      const float amax = __builtin_amdgcn_exp2f(bmine * pa.l2s - m);
+      const float amax = __builtin_amdgcn_exp2f(bs - m);
       const unsigned ab = __float_as_uint(amax);
       // OCP: floor(log2 amax) - 2; scale6: ceil(log2(amax / 6)), which is
       // floor(log2 amax) - 2, plus one when the mantissa exceeds 1.5
@@ -230,7 +235,7 @@ __device__ __forceinline__ bool pg_params(float pm0, float pm1, float& m, const 
       st.w[0] = st.w[1] = st.w[2] = st.w[3] = 0u;
     } else {
       // Alg. 1: M_b = max_t x_t = fl(fl(max acc * scale) - m)
-      const float Mb = bmine * pa.scale - m;
+      const float Mb = bs - m;
       // k_b = floor((M_b + log(2/9)) / log 2), Eq. (k-rule); -inf -> INT_MIN -> -127
       int kb = cvt_flr((Mb + kLog29) * kInvLn2);
       kb = kb < -127 ? -127 : kb;
@@ -341,11 +346,19 @@ __device__ __forceinline__ PgenOut pg_finish(PgenState& st) {
   return o;
 }
 
+// Element pair of pair slot S (0..15): dword S / 4, its pairs taken in the
+// order elements 0-1, 4-5, 2-3, 6-7, so that consecutive slots extend the
+// two byte chains d[0] and d[1] of the dword in turn (two independent
+// dependency chains instead of one; for exp-then-quantize, whose pairs 0-1
+// and 2-3 carry all the conversions, an even spread over the regions).
+__host__ __device__ constexpr int slot_elem(int S) { return 8 * (S >> 2) + ((S & 1) << 2) + (S & 2); }
+
+// Pair slots E0 / 2 .. E1 / 2 - 1.
 template <int KIND, int E0, int E1>
 __device__ __forceinline__ void pg_pairs(const f32x16& s0, const f32x16& s1, const PgenArgs& pa,
                                          PgenState& st) {
   if constexpr (E0 < E1) {
-    pg_pair<KIND, E0>(s0, s1, pa, st);
+    pg_pair<KIND, slot_elem(E0 / 2)>(s0, s1, pa, st);
     pg_pairs<KIND, E0 + 2, E1>(s0, s1, pa, st);
   }
 }
