@@ -62,3 +62,19 @@ def test_trace_and_counter_views_only_for_matching_source(tmp_path):
         f.write_text(f.read_text().replace(h, "0000000000000000"))
     assert bench.read_trace_avg_ms("w", str(d)) is None
     assert bench.read_stage_counters("w", str(d)) is None
+
+
+def test_committed_summaries_describe_the_committed_kernel():
+    # the trace, counter and traffic summaries under profiles/ were measured
+    # on the kernel source as committed: bench.py reports their figures only
+    # while the hash matches, so a kernel change without new summaries would
+    # silently drop them from the measurement line
+    d = os.path.join(os.path.dirname(bench.__file__), "profiles")
+    h = bench.kernel_hash()
+    for name in ("attn_pp_kernel_qwen3_8b_32k_stats.txt", "attn_pp_kernel_qwen3_8b_32k_counters.txt",
+                 "attn_fwd_qwen3_8b_32k_traffic.txt"):
+        lines = open(os.path.join(d, name)).read().splitlines()
+        assert f"kernel_hash = {h}" in lines, name
+    assert bench.read_trace_avg_ms("qwen3_8b_32k", d) is not None
+    assert bench.read_stage_counters("qwen3_8b_32k", d) is not None
+    assert bench.read_traffic("qwen3_8b_32k", d) is not None
