@@ -92,12 +92,14 @@ def _unpack(codes_u8):
     return np.stack([c & 0xF, c >> 4], axis=-1).reshape(*c.shape[:-1], -1)
 
 
-# Deep shapes (18-24 key tiles per wave): every ring slot is refilled
-# several times.
+# Deep shapes (18-24 key tiles per wave in the first three): every ring slot is refilled
+# several times; the last, two batches causal under the XCD-grouped work
+# order (24 work items).
 DEEP = [
     (1, 1100, 1100, 8, 2, 128, True),
     (1, 64, 1500, 4, 1, 64, False),
     (1, 300, 1300, 2, 2, 128, False),
+    (2, 520, 520, 4, 2, 128, True),
 ]
 
 

@@ -124,14 +124,18 @@ EDGE = [
 ]
 
 
-# Deep shapes: each wave streams 18-24 key tiles, so every slot of the K
-# ring (6 tiles) and the V~ ring (7 tiles) is refilled several times under
-# the four-tiles-ahead schedule: causal with grouped-query ratio 4, a
-# ragged tail past 23 full tiles, and seq_q < seq_k over 21 tiles.
+# Deep shapes: in the first three each wave streams 18-24 key tiles, so
+# every slot of the K ring (6 tiles) and the V~ ring (7 tiles) is refilled
+# several times under the four-tiles-ahead schedule: causal with
+# grouped-query ratio 4, a ragged tail past 23 full tiles, and seq_q < seq_k
+# over 21 tiles.  The last runs two batches causal with a ragged tail past
+# 8 tiles under the XCD-grouped work order (24 work items, a multiple of
+# the 8 XCDs).
 DEEP = [
     (1, 1100, 1100, 8, 2, 128, True),
     (1, 64, 1500, 4, 1, 64, False),
     (1, 300, 1300, 2, 2, 128, False),
+    (2, 520, 520, 4, 2, 128, True),
 ]
 
 
