@@ -88,3 +88,43 @@ def test_fullsize_sampled_rows(B, orc, wl):
                   f"{np.median(err):.2e}, over tol {bad.sum()}", flush=True)
             assert bad.sum() <= MAX_FLIP_ROWS * len(rows), (wl, kind)
             assert np.median(err) <= TOL / 4, (wl, kind)
+
+
+@pytest.mark.parametrize("wl", ["qwen3_8b_16k", "qwen3_8b_32k", "qwen3_8b_128k", "qwen3_vl_32k",
+                                "wan22_75600"])
+def test_fullsize_all_rows_in_value_hull(B, wl):
+    """Every row at full size, by a property that holds at any size: P~ >= 0
+    and O = (P~ V~) / (P~ 1), so each output element lies between the
+    smallest and the largest dequantised V~ value of that column over the
+    row's visible keys (a prefix for causal rows).  Catches a wrong kv head,
+    batch, key range or visibility anywhere in the grid, which sampled rows
+    can miss."""
+    w = inputs.WORKLOADS[wl]
+    print(f"[hull] {wl}", flush=True)
+    dev = torch.device("cuda:0")
+    q, k, v = inputs.make_qkv(w, device=dev)
+    vh = B.quant_v(v, seq_q=w.seq, heads_q=w.heads_q)
+    codes, e8 = B.vhat_natural(vh, B.shape_of(q, k))          # [Bt, Hkv, Skp, D], [Bt, Hkv, nb, D]
+    c8 = torch.tensor([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0], device=dev)
+    c = codes.long()
+    vq = c8[c & 7] * (1.0 - 2.0 * ((c >> 3) & 1).float())
+    del c, codes
+    vq = (vq * torch.exp2(e8.float() - 127.0).repeat_interleave(32, dim=2))[:, :, :w.seq]
+    if w.causal:
+        lo, hi = torch.cummin(vq, dim=2).values, torch.cummax(vq, dim=2).values
+    else:
+        lo, hi = vq.amin(dim=2, keepdim=True), vq.amax(dim=2, keepdim=True)
+    del vq
+    group = w.heads_q // w.heads_kv
+    for kind in ("efq", "expq"):
+        out = B.attn_fwd_vhat(q, k, vh, w.scale, w.causal, kind)
+        torch.cuda.synchronize()
+        worst = 0.0
+        for hq in range(w.heads_q):
+            o = out[:, :, hq, :]                                 # [Bt, S, D]
+            g = hq // group
+            over = torch.clamp(o - hi[:, g], min=0) + torch.clamp(lo[:, g] - o, min=0)
+            worst = max(worst, float(over.max()))
+        print(f"[hull] {wl} {kind}: largest step outside the hull {worst:.2e}", flush=True)
+        assert worst <= 1e-4, (wl, kind, worst)
+        del out
