@@ -122,6 +122,22 @@ def read_stage_counters(workload: str, profiles_dir: str = None):
             "speedup": round(1.0 - se / sx, 4) if sx > 0 else None}
 
 
+def read_stage_stamps(workload: str, profiles_dir: str = None):
+    """Probability-stage ticks per tile from the committed phase-stamp
+    summary (diagnostic build of the same kernel source): the matrix- plus
+    VALU-phase time above the no-op stage, and 1 - t_EFQ / t_EXPQ, or None."""
+    kv = read_profile(os.path.join(_profiles(profiles_dir),
+                                   f"attn_pp_kernel_{workload}_phases.txt"))
+    try:
+        efq, expq = (float(kv[f"stamps_stage_ticks_{k}"]) for k in ("efq", "expq"))
+        speedup = float(kv["stamps_speedup"])
+    except (TypeError, KeyError, ValueError):
+        return None
+    return {"unit": "s_memtime ticks per tile and wave above the no-op stage (phase stamps, "
+                    "diagnostic build)",
+            "efq": round(efq), "expq": round(expq), "speedup": round(speedup, 4)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -318,6 +334,7 @@ def main():
             "exposed_speedup": (round(1.0 - exposed["efq"] / exposed["expq"], 4)
                                 if exposed.get("expq", 0) > 0 else None),
             "stage_valu_counters": read_stage_counters(w.name),
+            "stage_stamps": read_stage_stamps(w.name),
             "paper_context": "Ascend 950PR vector-stage latency reduction 40.33% (16K-128K)",
         }
         result["policies"] = extra

@@ -553,6 +553,21 @@ struct AttnArgs {
 // at pp_schedule).  With MXFP8 Q and K (Q8) a K tile holds E4M3 codes in the
 // order the FP8 MFMA reads its A operand (see KLoad8), then 256 bytes of
 // E8M0 scales.
+// Phase stamps, a diagnostic build only (EFQ_PHASE_STAMPS=1, its own
+// library): the two waves of SIMD 0 in each of the first 256 workgroups
+// record s_memtime at the end of each of their first kStampPhases phases,
+// before and after the phase's wait and barrier, into LDS past the rings;
+// the kernel copies them out at its end.  Reading the counter makes the
+// wave wait for its outstanding LDS and scalar memory operations, so the
+// stamped kernel runs slower than the product build; the stamps give the
+// cycle distribution of the phases, not the product kernel's time.
+#ifndef EFQ_PHASE_STAMPS
+#define EFQ_PHASE_STAMPS 0
+#endif
+constexpr int kStampPhases = 512;
+constexpr int kStampBlocks = 256;
+constexpr int kStampBytes = EFQ_PHASE_STAMPS ? 2 * kStampPhases * 2 * 8 : 0;
+
 template <int D, int KS, int VS, bool Q8 = false>
 struct Smem {
   static constexpr int kK = Q8 ? kBc * D + 256 : kBc * D * 2;   // one K tile
@@ -561,7 +576,8 @@ struct Smem {
   static constexpr int kV = kVc + kVs;                   // one V~ tile
   static constexpr int kKOff = 0;
   static constexpr int kVOff = KS * kK;
-  static constexpr int kTotal = KS * kK + VS * kV;
+  static constexpr int kStampOff = KS * kK + VS * kV;
+  static constexpr int kTotal = KS * kK + VS * kV + kStampBytes;
 };
 
 // Direct-to-LDS loads (buffer_load ... lds: LDS address = M0 base + size *
@@ -1240,6 +1256,10 @@ __device__ __forceinline__ int ring_next(int off) {
   return off == STEP * DEPTH ? 0 : off;
 }
 
+#if EFQ_PHASE_STAMPS
+__device__ unsigned long long* g_stamps;   // [kStampBlocks][2 groups][kStampPhases][2]
+#endif
+
 template <int G, int D, int KIND, bool DUMP, bool Q8, typename Stream>
 __device__ __forceinline__ void pp_schedule(PPWave<D, KIND, DUMP, Q8>& w, int T, int ntiles,
                                             const uint8_t* kbuf0, const uint8_t* vbuf0,
@@ -1262,8 +1282,17 @@ __device__ __forceinline__ void pp_schedule(PPWave<D, KIND, DUMP, Q8>& w, int T,
     constexpr int TM = decltype(tm)::value;
     if constexpr (!kLate && (TM == 0 || TM == 2)) stream();
   };
+#if EFQ_PHASE_STAMPS
+  unsigned long long* const stamp =
+      (unsigned long long*)(const_cast<uint8_t*>(kbuf0) + Sm::kStampOff) + G * kStampPhases * 2;
+  const bool stamper = (threadIdx.x & 255) == 0;   // lane 0 of waves 0 and 4 (SIMD 0)
+  int ph = 0;
+#endif
   auto end = [&](auto tm) {
     constexpr int TM = decltype(tm)::value;
+#if EFQ_PHASE_STAMPS
+    if (stamper && ph < kStampPhases) stamp[2 * ph] = __builtin_amdgcn_s_memtime();
+#endif
     if constexpr (kLate && (TM == 0 || TM == 2)) {
       __builtin_amdgcn_sched_barrier(0);
       stream();
@@ -1276,6 +1305,10 @@ __device__ __forceinline__ void pp_schedule(PPWave<D, KIND, DUMP, Q8>& w, int T,
     } else {
       __builtin_amdgcn_sched_barrier(0);
     }
+#if EFQ_PHASE_STAMPS
+    if (stamper && ph < kStampPhases) stamp[2 * ph + 1] = __builtin_amdgcn_s_memtime();
+    ++ph;
+#endif
   };
   constexpr int TA = (2 + G) & 3, TB = (3 + G) & 3, TC = G, TD = (1 + G) & 3;
   // M(0), V(0) (group 1 after an empty phase); every later M(j) with Q K^T
@@ -1464,6 +1497,14 @@ attn_pp_kernel(const void* __restrict__ q, const void* __restrict__ k,
   else
     pp_schedule<1>(w, wtiles, ntiles, kbuf0, vbuf0, a, b, hq, keep, stream);
   wait_vmem();   // no load may still target LDS when the wave leaves
+#if EFQ_PHASE_STAMPS
+  if (g_stamps && blockIdx.x < kStampBlocks && (threadIdx.x & 255) == 0) {
+    const unsigned long long* src =
+        (const unsigned long long*)(smem + Sm::kStampOff) + group * kStampPhases * 2;
+    unsigned long long* dst = g_stamps + ((long)blockIdx.x * 2 + group) * kStampPhases * 2;
+    for (int i = 0; i < kStampPhases * 2; ++i) dst[i] = src[i];
+  }
+#endif
 
   // O = A / l as A * (1 / l): one division per row instead of one per
   // element (within 1.5 ulp of the quotient).  l = 0 only when every code of
@@ -1880,6 +1921,16 @@ int check_scale(float scale) {
 
 // ================================================================== C ABI
 extern "C" {
+
+#if EFQ_PHASE_STAMPS
+// Diagnostic build only: where the stamped kernel writes its phase stamps
+// (device buffer of kStampBlocks * 2 * kStampPhases * 2 uint64, zeroed by the
+// caller; phases a wave does not reach stay 0), or NULL for none.
+int efq_phase_stamps_set(void* buf) {
+  unsigned long long* p = (unsigned long long*)buf;
+  return hipMemcpyToSymbol(HIP_SYMBOL(g_stamps), &p, sizeof(p)) == hipSuccess ? EFQ_OK : EFQ_EHIP;
+}
+#endif
 
 int efq_abi_version(void) { return EFQ_ABI_VERSION; }
 

@@ -1,0 +1,166 @@
+"""Phase-stamp view of the fused attention kernel (the survey's in-kernel
+stamp method for the probability stage).
+
+usage: python3 -m paper_2609_09721_amd.phases [--workload qwen3_8b_32k] [--out FILE]
+
+Loads the diagnostic build libefq_attn_stamps.so (the same kernel source
+with EFQ_PHASE_STAMPS=1; build it beforehand with
+paper_2609_09721_amd.build.build_stamps) and runs the fused kernel on one
+workload for the EFQ, exp-then-quantize, EFQ-LUT and no-op stages.  The two
+waves of SIMD 0 in each of the first 256 workgroups stamp the end of every
+phase (work done, then wait and barrier done), which gives per phase:
+
+  work  from the previous phase's end to this phase's work end
+  wait  this phase's wait on its loads and, every fourth phase, the barrier
+
+A matrix phase M(j) holds the Q K^T MFMAs of tile j and the code step of
+tile j-1; a VALU phase V(j) the mask, maxima, parameters and rescale of
+tile j (the P~V MFMAs may sit in either, where the compiler put them).  Per
+tile a wave runs one of each, so the stage's own time per tile is
+(M + V)(stage) - (M + V)(no-op), medians over the steady-state phases, and
+the speedup 1 - t_EFQ / t_EXPQ (the paper's Table VIII definition).
+
+Reading the counter makes a wave wait for its outstanding LDS and scalar
+memory operations, so the stamped kernel is slower than the product build;
+the summary records both kernel times.  Ticks are s_memtime units.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import os
+import sys
+
+import numpy as np
+import torch
+
+from . import binding, build, inputs
+
+NBLK, NPH = 256, 512          # workgroups and phases stamped (kStampBlocks, kStampPhases)
+SKIP = 8                      # leading phases left out (prologue)
+KINDS = ("efq", "expq", "lut", "noop")
+
+
+def _load():
+    if not os.path.exists(build.STAMPS_LIB):
+        raise RuntimeError(f"{build.STAMPS_LIB} is missing: run build.build_stamps() first")
+    binding._lib = None
+    binding.LIB_PATH = build.STAMPS_LIB
+    L = binding.lib()
+    L.efq_phase_stamps_set.argtypes = [ctypes.c_void_p]
+    L.efq_phase_stamps_set.restype = ctypes.c_int
+    return L
+
+
+def _time(fn, n=5):
+    for _ in range(2):
+        fn()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    st = torch.cuda.current_stream()
+    for a, b in ev:
+        a.record(st)
+        fn()
+        b.record(st)
+    torch.cuda.synchronize()
+    return float(np.median([a.elapsed_time(b) for a, b in ev]))
+
+
+def phase_stats(t: np.ndarray) -> dict:
+    """t: [blocks, 2 groups, phases, 2] stamps.  Group g runs M(j) in phase
+    2j + g and V(j) in phase 2j + 1 + g."""
+    work = {"M": [], "V": []}
+    wait = {"M": [], "V": []}
+    for g in (0, 1):
+        x = t[:, g]
+        for p in range(SKIP, NPH - 2):
+            ok = (x[:, p - 1, 1] > 0) & (x[:, p, 0] > 0) & (x[:, p, 1] > 0)
+            kind = "M" if (p - g) % 2 == 0 else "V"
+            work[kind].append((x[ok, p, 0] - x[ok, p - 1, 1]))
+            wait[kind].append((x[ok, p, 1] - x[ok, p, 0]))
+    out = {}
+    for k in ("M", "V"):
+        w = np.concatenate(work[k]).astype(np.float64)
+        z = np.concatenate(wait[k]).astype(np.float64)
+        out[k] = {"n": int(w.size), "median": float(np.median(w)), "mean": float(w.mean()),
+                  "p90": float(np.percentile(w, 90)), "wait_median": float(np.median(z)),
+                  "wait_mean": float(z.mean())}
+    return out
+
+
+def measure(workload: str):
+    L = _load()
+    w = inputs.WORKLOADS[workload]
+    dev = torch.device("cuda:0")
+    q, k, v = inputs.make_qkv(w, device=dev)
+    vh = binding.quant_v(v, seq_q=w.seq, heads_q=w.heads_q)
+    out = torch.empty(q.shape, dtype=torch.float32, device=dev)
+    buf = torch.zeros(NBLK * 2 * NPH * 2, dtype=torch.int64, device=dev)
+    res = {}
+    for kind in KINDS:
+        print(f"[phases] {workload} {kind}", flush=True)
+        assert L.efq_phase_stamps_set(None) == 0
+        fn = lambda: binding.attn_fwd_vhat(q, k, vh, w.scale, w.causal, kind, out=out)
+        ms = _time(fn)
+        buf.zero_()
+        assert L.efq_phase_stamps_set(ctypes.c_void_p(buf.data_ptr())) == 0
+        fn()
+        torch.cuda.synchronize()
+        assert L.efq_phase_stamps_set(None) == 0
+        t = buf.cpu().numpy().reshape(NBLK, 2, NPH, 2)
+        res[kind] = {"ms": ms, **phase_stats(t)}
+    return res
+
+
+def summarize(res: dict, workload: str, command: str, kernel_hash: str) -> str:
+    lines = [
+        "# phase stamps of the fused attention kernel (diagnostic build with EFQ_PHASE_STAMPS=1), "
+        f"{workload}, bf16 Q K^T",
+        "# command (from the repository root, after paper_2609_09721_amd.build.build_stamps()):",
+        f"#   {command}",
+        "# two waves of SIMD 0 in each of the first 256 workgroups, phases "
+        f"{SKIP}..{NPH - 3} of each wave; ticks = s_memtime units",
+        "# work: previous phase end -> this phase's work end; wait: load wait and barrier",
+        "# stage per tile = median(M work) + median(V work) - the same for the no-op stage; "
+        "speedup = 1 - stage(EFQ) / stage(exp-then-quantize)",
+        "# stage | stamped kernel ms | M work median | M work mean | M work p90 | M wait median | "
+        "V work median | V work mean | V work p90 | V wait median | stage ticks per tile",
+    ]
+    base = res["noop"]["M"]["median"] + res["noop"]["V"]["median"]
+    stage = {}
+    for kind in KINDS:
+        r = res[kind]
+        stage[kind] = r["M"]["median"] + r["V"]["median"] - base
+        lines.append(
+            f"{kind} | {r['ms']:.3f} | {r['M']['median']:.0f} | {r['M']['mean']:.0f} | "
+            f"{r['M']['p90']:.0f} | {r['M']['wait_median']:.0f} | {r['V']['median']:.0f} | "
+            f"{r['V']['mean']:.0f} | {r['V']['p90']:.0f} | {r['V']['wait_median']:.0f} | "
+            f"{stage[kind]:.0f}")
+    for kind in ("efq", "expq", "lut"):
+        lines.append(f"stamps_stage_ticks_{kind} = {stage[kind]:.0f}")
+    if stage["expq"] > 0:
+        lines.append(f"stamps_speedup = {1.0 - stage['efq'] / stage['expq']:.4f}")
+    lines.append(f"kernel_hash = {kernel_hash}")
+    return "\n".join(lines) + "\n"
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--workload", default="qwen3_8b_32k")
+    ap.add_argument("--out", default=None)
+    a = ap.parse_args(argv)
+    assert torch.cuda.is_available(), "the phase stamps need a GPU"
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    sys.path.insert(0, root)
+    import bench
+    res = measure(a.workload)
+    cmd = f"python3 -m paper_2609_09721_amd.phases --workload {a.workload} --out <FILE>"
+    text = summarize(res, a.workload, cmd, bench.kernel_hash())
+    if a.out:
+        with open(a.out, "w") as f:
+            f.write(text)
+    print(text, end="")
+
+
+if __name__ == "__main__":
+    main()

@@ -65,16 +65,38 @@ def test_trace_and_counter_views_only_for_matching_source(tmp_path):
 
 
 def test_committed_summaries_describe_the_committed_kernel():
-    # the trace, counter and traffic summaries under profiles/ were measured
+    # the trace, counter, traffic and phase-stamp summaries under profiles/ were measured
     # on the kernel source as committed: bench.py reports their figures only
     # while the hash matches, so a kernel change without new summaries would
     # silently drop them from the measurement line
     d = os.path.join(os.path.dirname(bench.__file__), "profiles")
     h = bench.kernel_hash()
     for name in ("attn_pp_kernel_qwen3_8b_32k_stats.txt", "attn_pp_kernel_qwen3_8b_32k_counters.txt",
-                 "attn_fwd_qwen3_8b_32k_traffic.txt"):
+                 "attn_fwd_qwen3_8b_32k_traffic.txt", "attn_pp_kernel_qwen3_8b_32k_phases.txt"):
         lines = open(os.path.join(d, name)).read().splitlines()
         assert f"kernel_hash = {h}" in lines, name
     assert bench.read_trace_avg_ms("qwen3_8b_32k", d) is not None
     assert bench.read_stage_counters("qwen3_8b_32k", d) is not None
     assert bench.read_traffic("qwen3_8b_32k", d) is not None
+    assert bench.read_stage_stamps("qwen3_8b_32k", d) is not None
+
+
+def test_stamp_summary_round_trip(tmp_path):
+    # the phase-stamp summary that paper_2609_09721_amd.phases writes is read
+    # back by bench.py only while it carries the current kernel hash
+    from paper_2609_09721_amd import phases
+    res = {k: {"ms": 1.0, "M": {"median": m, "mean": m, "p90": m, "wait_median": 10.0,
+                                "wait_mean": 10.0, "n": 1},
+               "V": {"median": v, "mean": v, "p90": v, "wait_median": 20.0, "wait_mean": 20.0,
+                     "n": 1}}
+           for k, m, v in (("efq", 1200.0, 600.0), ("expq", 1400.0, 900.0),
+                           ("lut", 1300.0, 650.0), ("noop", 700.0, 200.0))}
+    d = tmp_path / "profiles"
+    d.mkdir()
+    text = phases.summarize(res, "w", "cmd", bench.kernel_hash())
+    (d / "attn_pp_kernel_w_phases.txt").write_text(text)
+    got = bench.read_stage_stamps("w", str(d))
+    assert got["efq"] == 900 and got["expq"] == 1400
+    assert got["speedup"] == round(1 - 900 / 1400, 4)
+    (d / "attn_pp_kernel_w_phases.txt").write_text(text.replace(bench.kernel_hash(), "0" * 16))
+    assert bench.read_stage_stamps("w", str(d)) is None
