@@ -137,8 +137,10 @@ __host__ __device__ __forceinline__ int key_nibble(int t) {
 // The stage is split into pieces so the fused kernel can interleave them
 // with the matrix-core work of the next tile:
 //   pg_max     partial block maxima of the lane's 32 scores
-//   pg_params  row maximum, alpha, and the per-block parameters (Alg. 1:
+//   pg_params  row maximum, its change, and the per-block parameters (Alg. 1:
 //              M_b, k_b, and the affine bias; or the exp-then-quantize scale)
+//   pg_alpha   alpha from the change (the fused kernel forms it only when
+//              some row maximum of the wave moved)
 //   pg_pair<E> codes of elements E, E+1 (element e = 16 * window + register)
 //   pg_finish  one v_permlane32_swap per half-block: lane L keeps window L/32
 // pgen<KIND>() runs them in order (standalone kernel and probe).
@@ -165,7 +167,7 @@ struct PgenState {
   float sc[2];        // EXPQ: 2^k_b per window (fp32 scale of the conversion)
   float mq;           // EXPQ: running maximum in log2 units
   int scale_b;        // E8M0 of the lane's own block
-  float alpha;
+  float dm;           // m^{j-1} - m^j (0 when the maximum is unchanged)
   unsigned w[4];      // packed codes: window 0 regs 0-7, 8-15, window 1 ...
 };
 
@@ -191,7 +193,7 @@ __device__ __forceinline__ bool pg_params(float pm0, float pm1, float& m, const 
   bool moved = false;
   if constexpr (KIND == EFQ_PGEN_NOOP) {
     st.scale_b = 127 - 6;
-    st.alpha = 1.0f;
+    st.dm = 0.0f;
     st.w[0] = st.w[1] = st.w[2] = st.w[3] = 0x22222222u;
     return moved;
   } else {
@@ -207,11 +209,8 @@ __device__ __forceinline__ bool pg_params(float pm0, float pm1, float& m, const 
     const float mt = fmax_swapped(t0, t1);      // rowmax S^j
     // m is itself a maximum (or -inf), so no operand quieting is needed
     const float mnew = fmax_swapped(m, mt);
-    // alpha = exp(m^{j-1} - m^j), Eq. (alpha): exp2(0) = 1 exactly when the
-    // max is unchanged, exp2(-inf) = 0 on the first tile; m^j is finite from
-    // the first tile on (key 0 is visible to every query), so d is never NaN
-    const float d = LOG2 ? (m - mnew) : (m - mnew) * kInvLn2;
-    st.alpha = __builtin_amdgcn_exp2f(d);
+    // alpha (pg_alpha) is formed only where a row maximum moved
+    st.dm = m - mnew;
     moved = __builtin_amdgcn_ballot_w64(m != mnew) != 0ull;
     m = mnew;
     if constexpr (is_expq<KIND>()) {
@@ -333,6 +332,15 @@ __device__ __forceinline__ void pg_pair(const f32x16& s0, const f32x16& s1, cons
   }
 }
 
+// alpha = exp(m^{j-1} - m^j), Eq. (alpha): exp2(0) = 1 exactly when the
+// maximum is unchanged, exp2(-inf) = 0 on the first tile; m^j is finite from
+// the first tile on (key 0 is visible to every query), so dm is never NaN.
+template <int KIND>
+__device__ __forceinline__ float pg_alpha(const PgenState& st) {
+  if constexpr (KIND == EFQ_PGEN_NOOP) return 1.0f;
+  else return __builtin_amdgcn_exp2f(is_expq<KIND>() ? st.dm : st.dm * kInvLn2);
+}
+
 template <int KIND>
 __device__ __forceinline__ PgenOut pg_finish(PgenState& st) {
   PgenOut o;
@@ -342,7 +350,7 @@ __device__ __forceinline__ PgenOut pg_finish(PgenState& st) {
   }
   o.bop = u32x4{st.w[0], st.w[1], st.w[2], st.w[3]};
   o.scale_b = st.scale_b;
-  o.alpha = st.alpha;
+  o.alpha = pg_alpha<KIND>(st);
   return o;
 }
 
@@ -1217,9 +1225,10 @@ struct PPWave {
     float pm0, pm1;
     pg_max<KIND>(s0, s1, pm0, pm1);
     if (pg_params<KIND>(pm0, pm1, m, pa, st)) {
+      const float alpha = pg_alpha<KIND>(st);
 #pragma unroll
-      for (int s = 0; s < NS; ++s) oacc[s] *= st.alpha;
-      lacc[0] *= st.alpha;
+      for (int s = 0; s < NS; ++s) oacc[s] *= alpha;
+      lacc[0] *= alpha;
     }
   }
 };
