@@ -1215,12 +1215,12 @@ struct PPWave {
   // tile j+1.
   __device__ __forceinline__ void vphase(int j, const uint8_t* vbuf0, int vr, const uint8_t* kbuf0,
                                          int krn, f32x16& s0, f32x16& s1, VOps<D>& vop,
-                                         KPre<D, Q8>& kp) {
+                                         KPre<D, Q8>& kp, int mask_from) {
     if constexpr (kMPrio != kVPrio) __builtin_amdgcn_s_setprio(kVPrio);
     if constexpr (kPreOn) kp.read(kbuf0 + krn, lane);
     read_v<D>(lds_at(vlane + vr), lds_at(vslane + vr), vop);
     // some lane's visible keys end inside this tile
-    if ((j + 1) * kBc > __builtin_amdgcn_readfirstlane(vis_min))
+    if (j >= mask_from)
       mask_tile(s0, s1, vis_end4 - j * kBc);
     float pm0, pm1;
     pg_max<KIND>(s0, s1, pm0, pm1);
@@ -1320,34 +1320,38 @@ __device__ __forceinline__ void pp_schedule(PPWave<D, KIND, DUMP, Q8>& w, int T,
 #endif
   };
   constexpr int TA = (2 + G) & 3, TB = (3 + G) & 3, TC = G, TD = (1 + G) & 3;
+  // first tile in which some lane of the wave has keys past its visible
+  // ones ((j + 1) kBc > the wave's smallest visible-key count); uniform, so
+  // the test in every VALU phase is a scalar compare
+  const int mask_from = __builtin_amdgcn_readfirstlane(w.vis_min) / kBc;
   // M(0), V(0) (group 1 after an empty phase); every later M(j) with Q K^T
   // follows a V(j-1) that pre-read its first K operands (j < T)
   if constexpr (G == 0) {
     begin(IC<4>{}); w.template mphase<true, false, false>(0, kbuf0, kr, vop, kp, a, b, hq, sa0, sa1, sb0, sb1); end(IC<4>{});
     kr = knext(kr);
-    begin(IC<1>{}); w.vphase(0, vbuf0, vr, kbuf0, kr, sa0, sa1, vop, kp); end(IC<1>{});
+    begin(IC<1>{}); w.vphase(0, vbuf0, vr, kbuf0, kr, sa0, sa1, vop, kp, mask_from); end(IC<1>{});
   } else {
     begin(IC<4>{}); end(IC<4>{});
     begin(IC<1>{}); w.template mphase<true, false, false>(0, kbuf0, kr, vop, kp, a, b, hq, sa0, sa1, sb0, sb1); end(IC<1>{});
     kr = knext(kr);
-    begin(IC<2>{}); w.vphase(0, vbuf0, vr, kbuf0, kr, sa0, sa1, vop, kp); end(IC<2>{});
+    begin(IC<2>{}); w.vphase(0, vbuf0, vr, kbuf0, kr, sa0, sa1, vop, kp, mask_from); end(IC<2>{});
   }
   vr = vnext(vr);
   int j = 1;
   for (; j + 1 < T; j += 2) {
     begin(IC<TA>{}); w.template mphase<true, true, true>(j, kbuf0, kr, vop, kp, a, b, hq, sb0, sb1, sa0, sa1); end(IC<TA>{});
     kr = knext(kr);
-    begin(IC<TB>{}); w.vphase(j, vbuf0, vr, kbuf0, kr, sb0, sb1, vop, kp); end(IC<TB>{});
+    begin(IC<TB>{}); w.vphase(j, vbuf0, vr, kbuf0, kr, sb0, sb1, vop, kp, mask_from); end(IC<TB>{});
     vr = vnext(vr);
     begin(IC<TC>{}); w.template mphase<true, true, true>(j + 1, kbuf0, kr, vop, kp, a, b, hq, sa0, sa1, sb0, sb1); end(IC<TC>{});
     kr = knext(kr);
-    begin(IC<TD>{}); w.vphase(j + 1, vbuf0, vr, kbuf0, kr, sa0, sa1, vop, kp); end(IC<TD>{});
+    begin(IC<TD>{}); w.vphase(j + 1, vbuf0, vr, kbuf0, kr, sa0, sa1, vop, kp, mask_from); end(IC<TD>{});
     vr = vnext(vr);
   }
   if (j < T) {   // one more tile: its scores go to set b, the last coded from b
     begin(IC<TA>{}); w.template mphase<true, true, true>(j, kbuf0, kr, vop, kp, a, b, hq, sb0, sb1, sa0, sa1); end(IC<TA>{});
     kr = knext(kr);
-    begin(IC<TB>{}); w.vphase(j, vbuf0, vr, kbuf0, kr, sb0, sb1, vop, kp); end(IC<TB>{});
+    begin(IC<TB>{}); w.vphase(j, vbuf0, vr, kbuf0, kr, sb0, sb1, vop, kp, mask_from); end(IC<TB>{});
     begin(IC<TC>{}); w.template mphase<false, true, false>(T, kbuf0, kr, vop, kp, a, b, hq, sa0, sa1, sb0, sb1); end(IC<TC>{});
   } else {       // the last tile's scores are in set a
     begin(IC<TA>{}); w.template mphase<false, true, false>(T, kbuf0, kr, vop, kp, a, b, hq, sb0, sb1, sa0, sa1); end(IC<TA>{});
