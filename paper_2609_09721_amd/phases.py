@@ -88,6 +88,32 @@ def phase_stats(t: np.ndarray) -> dict:
     return out
 
 
+def overlap(t: np.ndarray, grid: int = 4) -> tuple:
+    """Fraction of the stamped time in which at least one of the SIMD's two
+    waves, and in which both, are doing matrix-phase work (steady state of
+    each workgroup, sampled every `grid` ticks)."""
+    one = both = total = 0
+    for blk in range(t.shape[0]):
+        x = t[blk]
+        if (x[:, SKIP - 1:NPH - 1] == 0).any():
+            continue
+        lo = max(x[0, SKIP, 1], x[1, SKIP, 1])
+        hi = min(x[0, NPH - 2, 0], x[1, NPH - 2, 0])
+        if hi <= lo:
+            continue
+        g = np.arange(lo, hi, grid)
+        in_m = np.zeros((2, g.size), bool)
+        for grp in (0, 1):
+            for p in range(1, NPH - 1):
+                if (p - grp) % 2 == 0:
+                    i0, i1 = np.searchsorted(g, x[grp, p - 1, 1]), np.searchsorted(g, x[grp, p, 0])
+                    in_m[grp, i0:i1] = True
+        one += int((in_m[0] | in_m[1]).sum())
+        both += int((in_m[0] & in_m[1]).sum())
+        total += g.size
+    return (one / total, both / total) if total else (0.0, 0.0)
+
+
 def measure(workload: str):
     L = _load()
     w = inputs.WORKLOADS[workload]
@@ -109,6 +135,7 @@ def measure(workload: str):
         assert L.efq_phase_stamps_set(None) == 0
         t = buf.cpu().numpy().reshape(NBLK, 2, NPH, 2)
         res[kind] = {"ms": ms, **phase_stats(t)}
+        res[kind]["m_any"], res[kind]["m_both"] = overlap(t)
     return res
 
 
@@ -123,8 +150,11 @@ def summarize(res: dict, workload: str, command: str, kernel_hash: str) -> str:
         "# work: previous phase end -> this phase's work end; wait: load wait and barrier",
         "# stage per tile = median(M work) + median(V work) - the same for the no-op stage; "
         "speedup = 1 - stage(EFQ) / stage(exp-then-quantize)",
+        "# M any / M both: share of the stamped time in which at least one / both of a SIMD's two "
+        "waves do matrix-phase work",
         "# stage | stamped kernel ms | M work median | M work mean | M work p90 | M wait median | "
-        "V work median | V work mean | V work p90 | V wait median | stage ticks per tile",
+        "V work median | V work mean | V work p90 | V wait median | stage ticks per tile | "
+        "M any | M both",
     ]
     base = res["noop"]["M"]["median"] + res["noop"]["V"]["median"]
     stage = {}
@@ -135,7 +165,7 @@ def summarize(res: dict, workload: str, command: str, kernel_hash: str) -> str:
             f"{kind} | {r['ms']:.3f} | {r['M']['median']:.0f} | {r['M']['mean']:.0f} | "
             f"{r['M']['p90']:.0f} | {r['M']['wait_median']:.0f} | {r['V']['median']:.0f} | "
             f"{r['V']['mean']:.0f} | {r['V']['p90']:.0f} | {r['V']['wait_median']:.0f} | "
-            f"{stage[kind]:.0f}")
+            f"{stage[kind]:.0f} | {r.get('m_any', 0.0):.3f} | {r.get('m_both', 0.0):.3f}")
     for kind in ("efq", "expq", "lut"):
         lines.append(f"stamps_stage_ticks_{kind} = {stage[kind]:.0f}")
     if stage["expq"] > 0:
