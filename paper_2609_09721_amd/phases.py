@@ -1,5 +1,5 @@
-"""Phase-stamp view of the fused attention kernel (the survey's in-kernel
-stamp method for the probability stage).
+"""Phase-stamp view of the fused attention kernel: in-kernel timer stamps
+that time the probability stage inside the fused kernel.
 
 usage: python3 -m paper_2609_09721_amd.phases [--workload qwen3_8b_32k] [--out FILE]
 
