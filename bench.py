@@ -41,6 +41,7 @@ sys.path.insert(0, ROOT)
 PEAK_BF16 = 2500.0     # TFLOP/s, MI355X dense bf16 MFMA
 PEAK_FP4 = 10100.0     # TFLOP/s, MI355X dense MXFP4 MFMA
 PEAK_FP8 = 5000.0      # TFLOP/s, MI355X dense FP8 MFMA
+PEAK_CLOCK_GHZ = 2.4   # the clock the peaks are quoted at
 N_CU = 256
 COPY_BYTES = 1 << 30   # plain copy used to scale the HBM counters
 
@@ -133,9 +134,27 @@ def read_stage_stamps(workload: str, profiles_dir: str = None):
         speedup = float(kv["stamps_speedup"])
     except (TypeError, KeyError, ValueError):
         return None
-    return {"unit": "s_memtime ticks per tile and wave above the no-op stage (phase stamps, "
-                    "diagnostic build)",
-            "efq": round(efq), "expq": round(expq), "speedup": round(speedup, 4)}
+    out = {"unit": "s_memtime ticks (shader-clock cycles) per tile and wave above the no-op "
+                   "stage (phase stamps, diagnostic build)",
+           "efq": round(efq), "expq": round(expq), "speedup": round(speedup, 4)}
+    try:
+        out["sclk_ghz"] = float(kv["stamps_sclk_ghz"])
+    except (KeyError, ValueError):
+        pass
+    return out
+
+
+def measure_sclk(binding, stream, blocks: int = None, iters: int = 4000) -> float:
+    """Shader clock in GHz under a matrix-core load, taken right after the
+    timed steps: an MFMA stream on every CU (efq_clock_probe), s_memtime
+    ticks over s_memrealtime ticks (100 MHz), median over workgroups."""
+    import numpy as np
+    import torch
+    t = binding.clock_probe(blocks or N_CU, iters, stream=stream)
+    torch.cuda.synchronize()
+    a = t.cpu().numpy().astype(np.float64)
+    ok = a[:, 1] > 0
+    return float(np.median(0.1 * a[ok, 0] / a[ok, 1])) if ok.any() else 0.0
 
 
 def main():
@@ -248,6 +267,7 @@ def main():
         return
 
     ms_step, attn_ms, vq_ms, wall = timed(args.kind, args.steps, args.warmup)
+    sclk = measure_sclk(binding, stream)
     flops = w.flops()
     value = flops / (ms_step * 1e-3) / 1e12
     achieved = flops / (attn_ms * 1e-3) / 1e12
@@ -289,6 +309,11 @@ def main():
             "trace_median_ms": trace_ms[1] if trace_ms else None,
             "trace_frac": (round(flops / (trace_ms[0] * 1e-3) / 1e12 / peak, 4)
                            if trace_ms else None),
+            # the peaks are quoted at the 2.4 GHz peak clock; the clock the
+            # matrix cores ran at right after the timed steps, and the
+            # fraction of the peak scaled to it
+            "sclk_ghz": round(sclk, 3),
+            "frac_at_sclk": round(achieved / (peak * sclk / PEAK_CLOCK_GHZ), 4) if sclk > 0 else None,
         },
         "vquant_ms": round(vq_ms, 4),
     }

@@ -264,6 +264,17 @@ int efq_attn_fwd_dump(const void *q, const void *k, const void *vhat, size_t vha
 int efq_pgen_bench(int kind, efq_params p, int waves, int iters, uint32_t *checksum,
                    efq_stream_t stream);
 
+/* Shader-clock probe (diagnostic; the roofline peaks are quoted at the
+ * 2.4 GHz peak clock, and the clock the matrix cores actually run at under
+ * load sets what a kernel can reach).  `blocks` workgroups of four waves
+ * each stream bf16 32x32x16 MFMAs for iters x 16 MFMAs per wave; out
+ * (device, 2 x blocks uint64, caller-owned) receives per workgroup the
+ * s_memtime ticks (shader clock) and the s_memrealtime ticks (100 MHz) of
+ * the loop, so the clock in GHz is 0.1 x out[2i] / out[2i + 1].  blocks in
+ * [1, 65535], iters in [1, 2^20]; EFQ_EINVAL otherwise, before any HIP
+ * call. */
+int efq_clock_probe(int blocks, int iters, uint64_t *out, efq_stream_t stream);
+
 const char *efq_strerror(int status);
 
 /* ABI version of this header. */

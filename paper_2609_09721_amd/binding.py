@@ -66,6 +66,7 @@ SIGNATURES = {
     "efq_pgen": ([P, I, I, I, Params, P, P, P], I),
     "efq_attn_fwd_dump": ([P, P, P, SZ, F, I, I, Params, P, SP, P, P, P, P, P], I),
     "efq_pgen_bench": ([I, Params, I, I, P, P], I),
+    "efq_clock_probe": ([I, I, P, P], I),
     "efq_calibrate_workspace_bytes": ([SP, I], SZ),
     "efq_calibrate": ([P, P, P, F, I, P, SP, P, I, P, I, P, ctypes.POINTER(Params), P, SZ, P], I),
     "efq_qhat_bytes": ([SP], SZ),
@@ -385,6 +386,19 @@ def pgen_bench(kind="efq", params=None, waves: int = 4096, iters: int = 256,
     _check(lib().efq_pgen_bench(kind, _params(kind, params), int(waves), int(iters),
                                 _ptr(checksum), _stream(stream)))
     return checksum
+
+
+def clock_probe(blocks: int = 256, iters: int = 4000, out: Optional[torch.Tensor] = None,
+                stream=None) -> torch.Tensor:
+    """[blocks, 2] int64 on the GPU: per workgroup the s_memtime ticks (shader
+    clock) and the s_memrealtime ticks (100 MHz) of an MFMA stream (the
+    clock in GHz is 0.1 * col0 / col1); asynchronous on `stream`."""
+    if out is None:
+        out = torch.empty((blocks, 2), dtype=torch.int64, device="cuda")
+    if out.dtype != torch.int64 or not out.is_cuda or out.numel() < 2 * blocks or not out.is_contiguous():
+        raise ValueError("out must be a contiguous int64 CUDA tensor of at least 2 * blocks elements")
+    _check(lib().efq_clock_probe(int(blocks), int(iters), _ptr(out), _stream(stream)))
+    return out
 
 
 def unpack_nibbles(packed: torch.Tensor) -> torch.Tensor:

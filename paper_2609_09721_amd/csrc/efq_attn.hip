@@ -13,6 +13,7 @@
 //                      matrix-core and VALU phases.
 //   pgen_kernel        the probability stage alone on given shifted scores.
 //   pgen_bench_kernel  register-resident throughput probe of that stage.
+//   clock_probe_kernel shader clock under a matrix-core load (diagnostic).
 //   rho_partial_kernel, rho_final_kernel
 //                      the relative Frobenius error of Alg. 3's calibration
 //                      objective, in fp64 with a fixed reduction order.
@@ -565,16 +566,20 @@ struct AttnArgs {
 // library): the two waves of SIMD 0 in each of the first 256 workgroups
 // record s_memtime at the end of each of their first kStampPhases phases,
 // before and after the phase's wait and barrier, into LDS past the rings;
-// the kernel copies them out at its end.  Reading the counter makes the
-// wave wait for its outstanding LDS and scalar memory operations, so the
-// stamped kernel runs slower than the product build; the stamps give the
-// cycle distribution of the phases, not the product kernel's time.
+// the kernel copies them out at its end.  Four more slots per wave hold
+// s_memtime and s_memrealtime (100 MHz) at the end of its first and of its
+// last stamped phase, which gives the shader clock during the kernel.
+// Reading the counter makes the wave wait for its outstanding LDS and
+// scalar memory operations, so the stamped kernel runs slower than the
+// product build; the stamps give the cycle distribution of the phases, not
+// the product kernel's time.
 #ifndef EFQ_PHASE_STAMPS
 #define EFQ_PHASE_STAMPS 0
 #endif
 constexpr int kStampPhases = 512;
 constexpr int kStampBlocks = 256;
-constexpr int kStampBytes = EFQ_PHASE_STAMPS ? 2 * kStampPhases * 2 * 8 : 0;
+constexpr int kStampSlots = 2 * kStampPhases + 4;   // per wave: 2 per phase, then the clock pairs
+constexpr int kStampBytes = EFQ_PHASE_STAMPS ? 2 * kStampSlots * 8 : 0;
 
 template <int D, int KS, int VS, bool Q8 = false>
 struct Smem {
@@ -1266,7 +1271,7 @@ __device__ __forceinline__ int ring_next(int off) {
 }
 
 #if EFQ_PHASE_STAMPS
-__device__ unsigned long long* g_stamps;   // [kStampBlocks][2 groups][kStampPhases][2]
+__device__ unsigned long long* g_stamps;   // [kStampBlocks][2 groups][kStampSlots]
 #endif
 
 template <int G, int D, int KIND, bool DUMP, bool Q8, typename Stream>
@@ -1293,7 +1298,7 @@ __device__ __forceinline__ void pp_schedule(PPWave<D, KIND, DUMP, Q8>& w, int T,
   };
 #if EFQ_PHASE_STAMPS
   unsigned long long* const stamp =
-      (unsigned long long*)(const_cast<uint8_t*>(kbuf0) + Sm::kStampOff) + G * kStampPhases * 2;
+      (unsigned long long*)(const_cast<uint8_t*>(kbuf0) + Sm::kStampOff) + G * kStampSlots;
   const bool stamper = (threadIdx.x & 255) == 0;   // lane 0 of waves 0 and 4 (SIMD 0)
   int ph = 0;
 #endif
@@ -1315,7 +1320,14 @@ __device__ __forceinline__ void pp_schedule(PPWave<D, KIND, DUMP, Q8>& w, int T,
       __builtin_amdgcn_sched_barrier(0);
     }
 #if EFQ_PHASE_STAMPS
-    if (stamper && ph < kStampPhases) stamp[2 * ph + 1] = __builtin_amdgcn_s_memtime();
+    if (stamper && ph < kStampPhases) {
+      const unsigned long long mt = __builtin_amdgcn_s_memtime();
+      const unsigned long long rt = __builtin_amdgcn_s_memrealtime();
+      stamp[2 * ph + 1] = mt;
+      unsigned long long* const clk = stamp + 2 * kStampPhases + (ph == 0 ? 0 : 2);
+      clk[0] = mt;
+      clk[1] = rt;
+    }
     ++ph;
 #endif
   };
@@ -1513,9 +1525,9 @@ attn_pp_kernel(const void* __restrict__ q, const void* __restrict__ k,
 #if EFQ_PHASE_STAMPS
   if (g_stamps && blockIdx.x < kStampBlocks && (threadIdx.x & 255) == 0) {
     const unsigned long long* src =
-        (const unsigned long long*)(smem + Sm::kStampOff) + group * kStampPhases * 2;
-    unsigned long long* dst = g_stamps + ((long)blockIdx.x * 2 + group) * kStampPhases * 2;
-    for (int i = 0; i < kStampPhases * 2; ++i) dst[i] = src[i];
+        (const unsigned long long*)(smem + Sm::kStampOff) + group * kStampSlots;
+    unsigned long long* dst = g_stamps + ((long)blockIdx.x * 2 + group) * kStampSlots;
+    for (int i = 0; i < kStampSlots; ++i) dst[i] = src[i];
   }
 #endif
 
@@ -1633,6 +1645,43 @@ __global__ __launch_bounds__(256) void pgen_bench_kernel(int iters, float tau, f
     m = m - 0.25f + 0.5f * (float)(acc & 1u);
   }
   if (lane == 0) checksum[wid] = acc;
+}
+
+// ------------------------------------------------- shader clock probe
+// Every wave of a 256-thread workgroup streams bf16 32x32x16 MFMAs on two
+// independent accumulators (the matrix core at its full rate) for iters x 16
+// MFMAs; lane 0 of wave 0 stores the s_memtime ticks (shader clock) and the
+// s_memrealtime ticks (a constant 100 MHz) the loop took, so their ratio is
+// the shader clock under a matrix-core load.  The accumulators feed the
+// stored value through a test that never holds, so the loop stays.
+__global__ __launch_bounds__(256) void clock_probe_kernel(int iters,
+                                                          unsigned long long* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  bf16x8 x, y;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    x[i] = (__bf16)(0.001f * (float)(lane + i));
+    y[i] = (__bf16)(0.002f * (float)i);
+  }
+  f32x16 a0 = {}, a1 = {};
+  const unsigned long long m0 = __builtin_amdgcn_s_memtime();
+  const unsigned long long r0 = __builtin_amdgcn_s_memrealtime();
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      a0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, a0, 0, 0, 0);
+      a1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, a1, 0, 0, 0);
+    }
+  }
+  const unsigned long long m1 = __builtin_amdgcn_s_memtime();
+  const unsigned long long r1 = __builtin_amdgcn_s_memrealtime();
+  float sum = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) sum += a0[i] + a1[i];
+  if (threadIdx.x == 0) {
+    out[2 * blockIdx.x] = (m1 - m0) + (sum == -1.0f ? 1ull : 0ull);
+    out[2 * blockIdx.x + 1] = r1 - r0;
+  }
 }
 
 __global__ void fill_zero_kernel(uint8_t* __restrict__ p, size_t n) {
@@ -1937,7 +1986,7 @@ extern "C" {
 
 #if EFQ_PHASE_STAMPS
 // Diagnostic build only: where the stamped kernel writes its phase stamps
-// (device buffer of kStampBlocks * 2 * kStampPhases * 2 uint64, zeroed by the
+// (device buffer of kStampBlocks * 2 * kStampSlots uint64, zeroed by the
 // caller; phases a wave does not reach stay 0), or NULL for none.
 int efq_phase_stamps_set(void* buf) {
   unsigned long long* p = (unsigned long long*)buf;
@@ -2389,6 +2438,20 @@ int efq_pgen_bench(int kind, efq_params p, int waves, int iters, uint32_t* check
                        checksum, waves);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(EFQ_EHIP, "pgen bench launch: %s", hipGetErrorString(e));
+  return EFQ_OK;
+}
+
+int efq_clock_probe(int blocks, int iters, uint64_t* out, efq_stream_t stream) {
+  if (!out) return fail(EFQ_EINVAL, "null pointer");
+  if (blocks < 1 || blocks > 65535 || iters < 1 || iters > (1 << 20))
+    return fail(EFQ_EINVAL, "blocks must be in [1, 65535] and iters in [1, 2^20]");
+  int rc;
+  if ((rc = check_device())) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  hipLaunchKernelGGL(clock_probe_kernel, dim3((unsigned)blocks), dim3(256), 0, st, iters,
+                     (unsigned long long*)out);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(EFQ_EHIP, "clock probe launch: %s", hipGetErrorString(e));
   return EFQ_OK;
 }
 

@@ -22,7 +22,9 @@ the speedup 1 - t_EFQ / t_EXPQ (the paper's Table VIII definition).
 
 Reading the counter makes a wave wait for its outstanding LDS and scalar
 memory operations, so the stamped kernel is slower than the product build;
-the summary records both kernel times.  Ticks are s_memtime units.
+the summary records both kernel times.  Ticks are s_memtime units (shader
+clock cycles); each wave also records s_memrealtime (100 MHz) beside its
+first and last stamps, which gives the shader clock during the kernel.
 """
 from __future__ import annotations
 
@@ -37,6 +39,7 @@ import torch
 from . import binding, build, inputs
 
 NBLK, NPH = 256, 512          # workgroups and phases stamped (kStampBlocks, kStampPhases)
+SLOTS = 2 * NPH + 4           # per wave: two stamps per phase, then the two clock pairs
 SKIP = 8                      # leading phases left out (prologue)
 KINDS = ("efq", "expq", "lut", "noop")
 
@@ -114,6 +117,16 @@ def overlap(t: np.ndarray, grid: int = 4) -> tuple:
     return (one / total, both / total) if total else (0.0, 0.0)
 
 
+def sclk_ghz(clk: np.ndarray) -> float:
+    """clk: [blocks, 2 groups, 4] = (s_memtime, s_memrealtime) at the end of
+    a wave's first and of its last stamped phase; the median over waves of
+    the shader clock in GHz (s_memrealtime counts at 100 MHz)."""
+    c = clk.reshape(-1, 4).astype(np.float64)
+    dt, dr = c[:, 2] - c[:, 0], c[:, 3] - c[:, 1]
+    ok = (dr > 0) & (dt > 0)
+    return float(np.median(0.1 * dt[ok] / dr[ok])) if ok.any() else 0.0
+
+
 def measure(workload: str):
     L = _load()
     w = inputs.WORKLOADS[workload]
@@ -121,7 +134,7 @@ def measure(workload: str):
     q, k, v = inputs.make_qkv(w, device=dev)
     vh = binding.quant_v(v, seq_q=w.seq, heads_q=w.heads_q)
     out = torch.empty(q.shape, dtype=torch.float32, device=dev)
-    buf = torch.zeros(NBLK * 2 * NPH * 2, dtype=torch.int64, device=dev)
+    buf = torch.zeros(NBLK * 2 * SLOTS, dtype=torch.int64, device=dev)
     res = {}
     for kind in KINDS:
         print(f"[phases] {workload} {kind}", flush=True)
@@ -133,9 +146,11 @@ def measure(workload: str):
         fn()
         torch.cuda.synchronize()
         assert L.efq_phase_stamps_set(None) == 0
-        t = buf.cpu().numpy().reshape(NBLK, 2, NPH, 2)
+        x = buf.cpu().numpy().reshape(NBLK, 2, SLOTS)
+        t = x[:, :, :2 * NPH].reshape(NBLK, 2, NPH, 2)
         res[kind] = {"ms": ms, **phase_stats(t)}
         res[kind]["m_any"], res[kind]["m_both"] = overlap(t)
+        res[kind]["sclk"] = sclk_ghz(x[:, :, 2 * NPH:])
     return res
 
 
@@ -152,9 +167,11 @@ def summarize(res: dict, workload: str, command: str, kernel_hash: str) -> str:
         "speedup = 1 - stage(EFQ) / stage(exp-then-quantize)",
         "# M any / M both: share of the stamped time in which at least one / both of a SIMD's two "
         "waves do matrix-phase work",
+        "# SCLK: shader clock during the stamped kernel, s_memtime ticks over s_memrealtime "
+        "(100 MHz) between a wave's first and last stamped phase ends, median over waves",
         "# stage | stamped kernel ms | M work median | M work mean | M work p90 | M wait median | "
         "V work median | V work mean | V work p90 | V wait median | stage ticks per tile | "
-        "M any | M both",
+        "M any | M both | SCLK GHz",
     ]
     base = res["noop"]["M"]["median"] + res["noop"]["V"]["median"]
     stage = {}
@@ -165,11 +182,14 @@ def summarize(res: dict, workload: str, command: str, kernel_hash: str) -> str:
             f"{kind} | {r['ms']:.3f} | {r['M']['median']:.0f} | {r['M']['mean']:.0f} | "
             f"{r['M']['p90']:.0f} | {r['M']['wait_median']:.0f} | {r['V']['median']:.0f} | "
             f"{r['V']['mean']:.0f} | {r['V']['p90']:.0f} | {r['V']['wait_median']:.0f} | "
-            f"{stage[kind]:.0f} | {r.get('m_any', 0.0):.3f} | {r.get('m_both', 0.0):.3f}")
+            f"{stage[kind]:.0f} | {r.get('m_any', 0.0):.3f} | {r.get('m_both', 0.0):.3f} | "
+            f"{r.get('sclk', 0.0):.3f}")
     for kind in ("efq", "expq", "lut"):
         lines.append(f"stamps_stage_ticks_{kind} = {stage[kind]:.0f}")
     if stage["expq"] > 0:
         lines.append(f"stamps_speedup = {1.0 - stage['efq'] / stage['expq']:.4f}")
+    if res["efq"].get("sclk", 0.0) > 0:
+        lines.append(f"stamps_sclk_ghz = {res['efq']['sclk']:.3f}")
     lines.append(f"kernel_hash = {kernel_hash}")
     return "\n".join(lines) + "\n"
 

@@ -98,6 +98,11 @@ def test_bad_arguments(L):
     assert lib.efq_pgen(FAKE, 0, 64, 0, L.Params(-3.06, 2.3), FAKE, FAKE, None) == L.EFQ_EINVAL
     assert lib.efq_pgen(FAKE, 4, 64, 3, L.Params(-3.06, 2.3), FAKE, FAKE, None) == L.EFQ_EINVAL
     assert lib.efq_pgen_bench(0, L.Params(-3.06, 2.3), 0, 10, FAKE, None) == L.EFQ_EINVAL
+    assert lib.efq_clock_probe(0, 10, FAKE, None) == L.EFQ_EINVAL
+    assert lib.efq_clock_probe(65536, 10, FAKE, None) == L.EFQ_EINVAL
+    assert lib.efq_clock_probe(4, 0, FAKE, None) == L.EFQ_EINVAL
+    assert lib.efq_clock_probe(4, (1 << 20) + 1, FAKE, None) == L.EFQ_EINVAL
+    assert lib.efq_clock_probe(4, 10, None, None) == L.EFQ_EINVAL
     assert lib.efq_quant_v_mxfp4(FAKE, ctypes.byref(s), FAKE, 8, None) == L.EFQ_EWORKSPACE
     assert lib.efq_attn_fwd_ex(FAKE, FAKE, FAKE, 0.125, 0, 0, L.Params(-3.06, 2.3), FAKE,
                                ctypes.byref(s), None, 64, None) == L.EFQ_EWORKSPACE

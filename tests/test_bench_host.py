@@ -3,6 +3,8 @@ HBM-traffic summary to the code it was measured on (no GPU needed)."""
 import os
 import shutil
 
+import numpy as np
+
 import bench
 
 SRC = os.path.join(os.path.dirname(bench.__file__), "paper_2609_09721_amd", "csrc", "efq_attn.hip")
@@ -98,5 +100,22 @@ def test_stamp_summary_round_trip(tmp_path):
     got = bench.read_stage_stamps("w", str(d))
     assert got["efq"] == 900 and got["expq"] == 1400
     assert got["speedup"] == round(1 - 900 / 1400, 4)
+    assert "sclk_ghz" not in got                      # no clock pairs in res
+    res["efq"]["sclk"] = 2.0834
+    (d / "attn_pp_kernel_w_phases.txt").write_text(phases.summarize(res, "w", "cmd",
+                                                                    bench.kernel_hash()))
+    assert bench.read_stage_stamps("w", str(d))["sclk_ghz"] == 2.083
     (d / "attn_pp_kernel_w_phases.txt").write_text(text.replace(bench.kernel_hash(), "0" * 16))
     assert bench.read_stage_stamps("w", str(d)) is None
+
+
+def test_stamp_clock_pairs():
+    # (s_memtime, s_memrealtime) at a wave's first and last stamped phase end:
+    # 2.1e6 shader ticks over 1e5 ticks of the 100 MHz counter is 2.1 GHz;
+    # waves with no clock pair (zeros) are left out of the median
+    from paper_2609_09721_amd import phases
+    clk = np.zeros((4, 2, 4), dtype=np.int64)
+    clk[:3, :, 0], clk[:3, :, 1] = 1000, 500
+    clk[:3, :, 2], clk[:3, :, 3] = 1000 + 2_100_000, 500 + 100_000
+    clk[0, 0, 2] = 1000 + 1_900_000
+    assert abs(phases.sclk_ghz(clk) - 2.1) < 1e-12

@@ -289,3 +289,27 @@ def test_calibrate_recovers_generating_point(B):
     assert (tg, hg) == (float(np.float32(-2.6)), float(np.float32(1.9)))
     assert rho[2, 0] == 0.0 and np.sum(rho == 0.0) == 1
 
+
+
+def test_clock_probe(B):
+    """The diagnostic shader-clock probe: per workgroup the s_memtime ticks
+    (shader clock) and the s_memrealtime ticks (100 MHz) of an MFMA stream.
+    One workgroup of four waves per CU puts one wave on each SIMD, whose 16
+    bf16 32x32x16 MFMAs per iteration take at least 32 shader cycles each;
+    the real-time span lies inside the event-timed launch, and the clock the
+    two give is a plausible MI355X shader clock."""
+    blocks, iters = 64, 2000
+    st = torch.cuda.current_stream()
+    B.clock_probe(blocks, 10)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(st)
+    t = B.clock_probe(blocks, iters)
+    e1.record(st)
+    torch.cuda.synchronize()
+    a = t.cpu().numpy().astype(np.float64)
+    assert (a > 0).all()
+    assert (a[:, 0] >= iters * 16 * 31).all(), a[:, 0].min()
+    assert a[:, 1].max() * 1e-5 <= e0.elapsed_time(e1) * 1.02 + 0.01
+    ghz = 0.1 * a[:, 0] / a[:, 1]
+    assert ((ghz > 0.5) & (ghz < 3.0)).all(), ghz
