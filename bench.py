@@ -267,6 +267,15 @@ def main():
         return
 
     ms_step, attn_ms, vq_ms, wall = timed(args.kind, args.steps, args.warmup)
+    kclk = None
+    if args.kind == "efq":
+        # the clock during the fused kernel on this machine: launches of the
+        # kernel's stamped diagnostic build (built beside the product
+        # library) right after the timed steps, before anything else runs
+        from paper_2609_09721_amd import build as hip_build, phases
+        if os.path.exists(hip_build.STAMPS_LIB):
+            kclk = round(phases.kernel_sclk(w, q, k, vhat, out), 3) or None
+            binding.lib()
     sclk = measure_sclk(binding, stream)
     flops = w.flops()
     value = flops / (ms_step * 1e-3) / 1e12
@@ -309,11 +318,14 @@ def main():
             "trace_median_ms": trace_ms[1] if trace_ms else None,
             "trace_frac": (round(flops / (trace_ms[0] * 1e-3) / 1e12 / peak, 4)
                            if trace_ms else None),
-            # the peaks are quoted at the 2.4 GHz peak clock; the clock the
-            # matrix cores ran at right after the timed steps, and the
-            # fraction of the peak scaled to it
-            "sclk_ghz": round(sclk, 3),
-            "frac_at_sclk": round(achieved / (peak * sclk / PEAK_CLOCK_GHZ), 4) if sclk > 0 else None,
+            # the peaks are quoted at the 2.4 GHz peak clock.  Shader clock
+            # during the kernel's stamped build right after the timed steps
+            # (median of 5 launches), of an MFMA-only stream after that, and
+            # the fraction of the peak scaled to the in-kernel clock
+            "sclk_ghz_mfma_probe": round(sclk, 3),
+            "sclk_ghz_in_kernel": kclk,
+            "frac_at_kernel_sclk": (round(achieved / (peak * kclk / PEAK_CLOCK_GHZ), 4)
+                                    if kclk else None),
         },
         "vquant_ms": round(vq_ms, 4),
     }

@@ -576,6 +576,9 @@ struct AttnArgs {
 #ifndef EFQ_PHASE_STAMPS
 #define EFQ_PHASE_STAMPS 0
 #endif
+#if EFQ_PHASE_STAMPS
+#define attn_pp_kernel attn_pp_kernel_stamped   // its own name in kernel traces
+#endif
 constexpr int kStampPhases = 512;
 constexpr int kStampBlocks = 256;
 constexpr int kStampSlots = 2 * kStampPhases + 4;   // per wave: 2 per phase, then the clock pairs

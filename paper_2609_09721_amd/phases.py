@@ -127,6 +127,30 @@ def sclk_ghz(clk: np.ndarray) -> float:
     return float(np.median(0.1 * dt[ok] / dr[ok])) if ok.any() else 0.0
 
 
+def kernel_sclk(w, q, k, vhat, out, kind: str = "efq", warm: int = 3, reps: int = 5) -> float:
+    """Shader clock (GHz) during the stamped build of the fused kernel on the
+    given inputs (a V~ from efq_quant_v_mxfp4 and an output buffer): `warm`
+    launches, then `reps` stamped ones back to back; the median of their
+    clocks.  The library binding.lib() returned before is restored after."""
+    saved = (binding._lib, binding.LIB_PATH)
+    try:
+        L = _load()
+        bufs = [torch.zeros(NBLK * 2 * SLOTS, dtype=torch.int64, device=q.device)
+                for _ in range(reps)]
+        for _ in range(warm):
+            binding.attn_fwd_vhat(q, k, vhat, w.scale, w.causal, kind, out=out)
+        for buf in bufs:
+            # the pointer is set by a blocking copy, after the launches before it
+            assert L.efq_phase_stamps_set(ctypes.c_void_p(buf.data_ptr())) == 0
+            binding.attn_fwd_vhat(q, k, vhat, w.scale, w.causal, kind, out=out)
+        torch.cuda.synchronize()
+        assert L.efq_phase_stamps_set(None) == 0
+        clk = [sclk_ghz(b.cpu().numpy().reshape(NBLK, 2, SLOTS)[:, :, 2 * NPH:]) for b in bufs]
+        return float(np.median(clk))
+    finally:
+        binding._lib, binding.LIB_PATH = saved
+
+
 def measure(workload: str):
     L = _load()
     w = inputs.WORKLOADS[workload]
