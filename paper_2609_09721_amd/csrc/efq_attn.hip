@@ -1520,6 +1520,14 @@ attn_pp_kernel(const void* __restrict__ q, const void* __restrict__ k,
   };
 
   constexpr int keep = kKeep * kLoads;
+#if EFQ_PHASE_STAMPS
+  // each stamping lane clears its own stamp area, so phases its wave does
+  // not reach read 0 rather than what an earlier workgroup left in LDS
+  if ((threadIdx.x & 255) == 0) {
+    unsigned long long* z = (unsigned long long*)(smem + Sm::kStampOff) + group * kStampSlots;
+    for (int i = 0; i < kStampSlots; ++i) z[i] = 0;
+  }
+#endif
   if (group == 0)
     pp_schedule<0>(w, wtiles, ntiles, kbuf0, vbuf0, a, b, hq, keep, stream);
   else

@@ -4,6 +4,7 @@ Bar: bit-exact E2M1 codes and E8M0 scales where the scores are bit-identical
 (the P-gen unit, and the fused kernel on exact-score inputs), attention
 output within 2e-3 max abs of the oracle's fp32 output.
 """
+import ctypes
 import math
 
 import numpy as np
@@ -313,3 +314,47 @@ def test_clock_probe(B):
     assert a[:, 1].max() * 1e-5 <= e0.elapsed_time(e1) * 1.02 + 0.01
     ghz = 0.1 * a[:, 0] / a[:, 1]
     assert ((ghz > 0.5) & (ghz < 3.0)).all(), ghz
+
+
+def test_stamped_build_matches_product(B):
+    """The phase-stamp diagnostic build (the bench's in-kernel clock and the
+    phase profile come from it) computes what the product build computes:
+    outputs bit-identical on a causal GQA shape of many tiles and a ragged
+    tail, for EFQ and the no-op stage; its clock pairs give a plausible
+    shader clock, and every workgroup it stamps records its first phases."""
+    from paper_2609_09721_amd import build as hip_build, phases
+    if not __import__("os").path.exists(hip_build.STAMPS_LIB):
+        pytest.skip("stamped build not built")
+    w = inputs.Workload("stamp", 1, 8, 2, 1100, 128, True, "normal", 4242)
+    q, k, v = inputs.make_qkv(w, device="cuda")
+    vh = B.quant_v(v, seq_q=w.seq, heads_q=w.heads_q)
+    ref = {kind: B.attn_fwd_vhat(q, k, vh, w.scale, True, kind) for kind in ("efq", "noop")}
+    torch.cuda.synchronize()
+    out = torch.empty_like(ref["efq"])
+    clk = phases.kernel_sclk(w, q, k, vh, out, "efq", warm=1, reps=2)
+    assert torch.equal(out, ref["efq"])
+    assert 0.5 < clk < 3.0, clk
+    saved = (B._lib, B.LIB_PATH)
+    try:
+        L = phases._load()
+        buf = torch.zeros(phases.NBLK * 2 * phases.SLOTS, dtype=torch.int64, device="cuda")
+        assert L.efq_phase_stamps_set(ctypes.c_void_p(buf.data_ptr())) == 0
+        B.attn_fwd_vhat(q, k, vh, w.scale, True, "noop", out=out)
+        torch.cuda.synchronize()
+        assert L.efq_phase_stamps_set(None) == 0
+        assert torch.equal(out, ref["noop"])
+    finally:
+        B._lib, B.LIB_PATH = saved
+    B.lib()
+    # 1100 queries of 8 heads: 40 workgroups of 256 queries (five per head).
+    # Every stamping wave stamps its first phase and its clock pairs; the
+    # stamps it takes only grow, the phases it does not reach read 0, and
+    # workgroups past the grid leave their rows untouched.
+    x = buf.cpu().numpy().reshape(phases.NBLK, 2, phases.SLOTS)
+    nwg = 8 * ((w.seq + 255) // 256)
+    assert (x[nwg:] == 0).all()
+    t = x[:nwg, :, :2 * phases.NPH].reshape(nwg * 2, -1)
+    assert (t[:, :2] > 0).all() and (x[:nwg, :, 2 * phases.NPH:] > 0).all()
+    for row in t:
+        n = int((row > 0).sum())
+        assert (row[:n] > 0).all() and (row[n:] == 0).all() and (np.diff(row[:n]) >= 0).all()
