@@ -267,7 +267,9 @@ int efq_pgen_bench(int kind, efq_params p, int waves, int iters, uint32_t *check
 /* Shader-clock probe (diagnostic; the roofline peaks are quoted at the
  * 2.4 GHz peak clock, and the clock the matrix cores actually run at under
  * load sets what a kernel can reach).  `blocks` workgroups of four waves
- * each stream bf16 32x32x16 MFMAs for iters x 16 MFMAs per wave; out
+ * each stream bf16 32x32x16 MFMAs, with operands that change every
+ * instruction, for iters x 16 MFMAs per wave (launches of a few
+ * milliseconds back to back give the clock the power limit holds); out
  * (device, 2 x blocks uint64, caller-owned) receives per workgroup the
  * s_memtime ticks (shader clock) and the s_memrealtime ticks (100 MHz) of
  * the loop, so the clock in GHz is 0.1 x out[2i] / out[2i + 1].  blocks in

@@ -1661,18 +1661,36 @@ __global__ __launch_bounds__(256) void pgen_bench_kernel(int iters, float tau, f
 // ------------------------------------------------- shader clock probe
 // Every wave of a 256-thread workgroup streams bf16 32x32x16 MFMAs on two
 // independent accumulators (the matrix core at its full rate) for iters x 16
-// MFMAs; lane 0 of wave 0 stores the s_memtime ticks (shader clock) and the
+// MFMAs, its operands rotating through four pseudo-random sets (signs,
+// exponents 2^-3 .. 2^4 and mantissas hashed from the lane, the workgroup
+// and the set) so that they change with every instruction as real data
+// does; lane 0 of wave 0 stores the s_memtime ticks (shader clock) and the
 // s_memrealtime ticks (a constant 100 MHz) the loop took, so their ratio is
 // the shader clock under a matrix-core load.  The accumulators feed the
 // stored value through a test that never holds, so the loop stays.
-__global__ __launch_bounds__(256) void clock_probe_kernel(int iters,
-                                                          unsigned long long* __restrict__ out) {
-  const int lane = threadIdx.x & 63;
-  bf16x8 x, y;
+__device__ __forceinline__ bf16x8 clock_probe_operand(unsigned seed) {
+  bf16x8 v;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    x[i] = (__bf16)(0.001f * (float)(lane + i));
-    y[i] = (__bf16)(0.002f * (float)i);
+    unsigned h = (seed + (unsigned)i * 0x9E3779B9u) * 0x85EBCA6Bu;
+    h ^= h >> 15;
+    h *= 0xC2B2AE35u;
+    h ^= h >> 13;
+    const unsigned short b = (unsigned short)(((h >> 31) << 15) | ((124u + ((h >> 20) & 7u)) << 7) |
+                                              (h & 0x7Fu));
+    v[i] = __builtin_bit_cast(__bf16, b);
+  }
+  return v;
+}
+
+__global__ __launch_bounds__(256) void clock_probe_kernel(int iters,
+                                                          unsigned long long* __restrict__ out) {
+  const unsigned seed = (blockIdx.x * 256u + threadIdx.x) * 8u;
+  bf16x8 x[4], y[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    x[s] = clock_probe_operand(seed + 2u * s);
+    y[s] = clock_probe_operand(seed + 2u * s + 1u);
   }
   f32x16 a0 = {}, a1 = {};
   const unsigned long long m0 = __builtin_amdgcn_s_memtime();
@@ -1680,8 +1698,8 @@ __global__ __launch_bounds__(256) void clock_probe_kernel(int iters,
   for (int it = 0; it < iters; ++it) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      a0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, a0, 0, 0, 0);
-      a1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, y, a1, 0, 0, 0);
+      a0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x[i & 3], y[i & 3], a0, 0, 0, 0);
+      a1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x[(i + 1) & 3], y[(i + 2) & 3], a1, 0, 0, 0);
     }
   }
   const unsigned long long m1 = __builtin_amdgcn_s_memtime();
