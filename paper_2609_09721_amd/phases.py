@@ -133,8 +133,11 @@ def kernel_sclk(w, q, k, vhat, out, kind: str = "efq", warm: int = 3, reps: int 
     launches, then `reps` stamped ones back to back; the median of their
     clocks.  The library binding.lib() returned before is restored after."""
     saved = (binding._lib, binding.LIB_PATH)
+    L = None
     try:
         L = _load()
+        # no stamp buffer from an earlier call may still be set
+        assert L.efq_phase_stamps_set(None) == 0
         bufs = [torch.zeros(NBLK * 2 * SLOTS, dtype=torch.int64, device=q.device)
                 for _ in range(reps)]
         for _ in range(warm):
@@ -148,11 +151,22 @@ def kernel_sclk(w, q, k, vhat, out, kind: str = "efq", warm: int = 3, reps: int 
         clk = [sclk_ghz(b.cpu().numpy().reshape(NBLK, 2, SLOTS)[:, :, 2 * NPH:]) for b in bufs]
         return float(np.median(clk))
     finally:
+        if L is not None:
+            torch.cuda.synchronize()
+            L.efq_phase_stamps_set(None)
         binding._lib, binding.LIB_PATH = saved
 
 
 def measure(workload: str):
     L = _load()
+    try:
+        return _measure(L, workload)
+    finally:
+        torch.cuda.synchronize()
+        L.efq_phase_stamps_set(None)
+
+
+def _measure(L, workload: str):
     w = inputs.WORKLOADS[workload]
     dev = torch.device("cuda:0")
     q, k, v = inputs.make_qkv(w, device=dev)
