@@ -124,7 +124,7 @@ __host__ __device__ __forceinline__ int nibble_key(int e) {
   return 8 * (r >> 2) + 4 * gq + (r & 3);
 }
 // Inverse: nibble position of key t (0..31).
-__host__ __device__ __forceinline__ int key_nibble(int t) {
+__host__ __device__ constexpr int key_nibble(int t) {
   return 8 * (2 * ((t >> 2) & 1) + (t >> 4)) + 2 * (t & 3) + ((t >> 3) & 1);
 }
 
@@ -396,33 +396,41 @@ __device__ __forceinline__ u32x4 unpermute_codes(const u32x4& bop) {
   return u32x4{out[0], out[1], out[2], out[3]};
 }
 
-__host__ __device__ __forceinline__ float bf16_bits_to_f32(unsigned short b) {
-#ifdef __HIP_DEVICE_COMPILE__
-  return __uint_as_float((unsigned)b << 16);
-#else
-  unsigned u = (unsigned)b << 16;
-  float f;
-  memcpy(&f, &u, 4);
-  return f;
-#endif
-}
-
 // ----------------------------------------------------------- V quantiser
 // One thread per (b, kv head, 32-key block, pair of columns).  OCP MX rule:
 // k = floor(log2 amax) - 2 (>= -127), codes RNE(|v| 2^-k) with saturation
-// at 6 and the bf16 sign bit, keys stored in FP4 operand order.
+// at 6 and the bf16 sign bit, keys stored in FP4 operand order.  The
+// rounding is the hardware FP4 conversion of v 2^-k at scale 1 (two keys
+// per instruction); the 32 row loads of a lane go out before any use.
 struct VqArgs {
   int B, S, H, D, nb;  // nb = padded number of 32-key blocks
   size_t scale_off;
+  unsigned vbytes;     // bytes of V when below 2^31 (buffer loads), else 0
 };
 
-__device__ __forceinline__ unsigned e2m1_rne(float y) {
-  // nearest E2M1 magnitude, ties to the even code, saturating at 6
-  unsigned c = (y > 0.25f) + (y >= 0.75f) + (y > 1.25f) + (y >= 1.75f) + (y > 2.5f) +
-               (y >= 3.5f) + (y > 5.0f);
-  return c;
+// Codes of keys T and T + 8 of the lane's column c (0: low bf16 half of the
+// raw dwords, 1: high) into byte T & 3 of dword 2 ((T >> 2) & 1) + (T >> 4),
+// for T = 0..7 and 16..23.
+template <int T>
+__device__ __forceinline__ void vq_pairs(unsigned (&words)[4], const unsigned (&raw)[32], int c,
+                                         int k) {
+  if constexpr (T < 24) {
+    if constexpr ((T & 8) == 0) {
+      const unsigned lo = c ? (raw[T] & 0xffff0000u) : (raw[T] << 16);
+      const unsigned hi = c ? (raw[T + 8] & 0xffff0000u) : (raw[T + 8] << 16);
+      const float y0 = ldexpf(__uint_as_float(lo), -k);
+      const float y1 = ldexpf(__uint_as_float(hi), -k);
+      constexpr int W = 2 * ((T >> 2) & 1) + (T >> 4);
+      static_assert(key_nibble(T) == 8 * W + 2 * (T & 3) && key_nibble(T + 8) == key_nibble(T) + 1,
+                    "keys T and T + 8 fill the low and high nibble of byte T & 3 of dword W");
+      words[W] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(words[W], y0, y1, 1.0f, T & 3);
+    }
+    vq_pairs<T + 1>(words, raw, c, k);
+  }
 }
 
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, unsigned bytes);
+template <bool BUF>
 __global__ __launch_bounds__(256) void vquant_kernel(const unsigned short* __restrict__ v,
                                                      uint8_t* __restrict__ vhat, VqArgs a) {
   const int D2 = a.D >> 1;
@@ -436,42 +444,47 @@ __global__ __launch_bounds__(256) void vquant_kernel(const unsigned short* __res
   int g = (int)(r % a.H);
   int b = (int)(r / a.H);
   const int d0 = 2 * dp;
-  float vals[2][32];
-  unsigned sgn[2] = {0u, 0u};
-  float amax0 = 0.f, amax1 = 0.f;
+  // the lane's column pair in the block's 32 rows; rows past S read as 0
+  const int nvalid = min(32, a.S - blk * 32);
+  const long e0 = (((long)b * a.S + (long)blk * 32) * a.H + g) * a.D + d0;
+  unsigned raw[32];
+  if constexpr (BUF) {
+    // one resource over V, the lane's row-0 offset in voffset and the row
+    // in the scalar offset: no per-row address arithmetic on the VALU
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(v, a.vbytes);
+    const unsigned voff = (unsigned)e0 * 2u;
+    const int sb = a.H * a.D * 2;   // bytes between consecutive keys
+#pragma unroll
+    for (int t = 0; t < 32; ++t)
+      raw[t] = t < nvalid ? __builtin_amdgcn_raw_buffer_load_b32(rs, voff, t * sb, 0) : 0u;
+  } else {
+    const unsigned* p = (const unsigned*)(v + e0);
+    const long stride = (long)a.H * a.D / 2;   // dwords between consecutive keys
+#pragma unroll
+    for (int t = 0; t < 32; ++t) raw[t] = t < nvalid ? p[t * stride] : 0u;
+  }
+  float amax[2] = {0.f, 0.f};
 #pragma unroll
   for (int t = 0; t < 32; ++t) {
-    int key = blk * 32 + t;
-    unsigned pair = 0;
-    if (key < a.S)
-      pair = *(const unsigned*)(v + (((long)b * a.S + key) * a.H + g) * a.D + d0);
-    unsigned short lo = (unsigned short)(pair & 0xFFFF), hi = (unsigned short)(pair >> 16);
-    sgn[0] |= (unsigned)(lo >> 15) << t;
-    sgn[1] |= (unsigned)(hi >> 15) << t;
-    vals[0][t] = fabsf(bf16_bits_to_f32(lo));
-    vals[1][t] = fabsf(bf16_bits_to_f32(hi));
-    amax0 = fmaxf(amax0, vals[0][t]);
-    amax1 = fmaxf(amax1, vals[1][t]);
+    amax[0] = fmaxf(amax[0], __uint_as_float((raw[t] & 0x7fffu) << 16));
+    amax[1] = fmaxf(amax[1], __uint_as_float(raw[t] & 0x7fff0000u));
   }
   uint8_t* codes = vhat + (((long)b * a.H + g) * a.nb + blk) * a.D * 16;
   uint8_t* scales = vhat + a.scale_off + (((long)b * a.H + g) * a.nb + blk) * a.D;
 #pragma unroll
   for (int c = 0; c < 2; ++c) {
-    float amax = c ? amax1 : amax0;
     int k = -127;
-    if (amax > 0.f) {
+    if (amax[c] > 0.f) {
       // floor(log2 amax) from the fp32 bits (bf16 subnormals are fp32 normals)
-      int e = (int)((__float_as_uint(amax) >> 23) & 0xFF) - 127;
+      int e = (int)((__float_as_uint(amax[c]) >> 23) & 0xFF) - 127;
       k = e - 2 < -127 ? -127 : e - 2;
     }
+    // keys t and t + 8 (t with bit 3 clear) share byte t & 3 of operand dword
+    // 2 ((t >> 2) & 1) + (t >> 4): key t in the low nibble (key_nibble);
+    // the conversion rounds y = v 2^-k (exact) to the nearest E2M1 value,
+    // ties to the even code, sign from the input
     unsigned words[4] = {0, 0, 0, 0};
-#pragma unroll
-    for (int t = 0; t < 32; ++t) {
-      float y = ldexpf(vals[c][t], -k);
-      unsigned code = e2m1_rne(y) | (((sgn[c] >> t) & 1u) << 3);
-      int e = key_nibble(t);
-      words[e >> 3] |= code << (4 * (e & 7));
-    }
+    vq_pairs<0>(words, raw, c, k);
     *(u32x4*)(codes + (long)(d0 + c) * 16) = u32x4{words[0], words[1], words[2], words[3]};
     const int d = d0 + c;
     scales[(d & 31) * (a.D >> 5) + (d >> 5)] = (uint8_t)(k + 127);
@@ -1860,8 +1873,14 @@ int launch_vquant(const void* v, const efq_shape* s, void* vhat, hipStream_t st)
   a.scale_off = vhat_scale_offset(s);
   long total = (long)a.B * a.H * a.nb * (a.D / 2);
   long grid = (total + 255) / 256;
-  hipLaunchKernelGGL(vquant_kernel, dim3((unsigned)grid), dim3(256), 0, st,
-                     (const unsigned short*)v, (uint8_t*)vhat, a);
+  const size_t vb = (size_t)a.B * a.S * a.H * a.D * 2;
+  a.vbytes = vb < ((size_t)1 << 31) ? (unsigned)vb : 0u;
+  if (a.vbytes)
+    hipLaunchKernelGGL(vquant_kernel<true>, dim3((unsigned)grid), dim3(256), 0, st,
+                       (const unsigned short*)v, (uint8_t*)vhat, a);
+  else
+    hipLaunchKernelGGL(vquant_kernel<false>, dim3((unsigned)grid), dim3(256), 0, st,
+                       (const unsigned short*)v, (uint8_t*)vhat, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(EFQ_EHIP, "vquant launch: %s", hipGetErrorString(e));
   return EFQ_OK;
