@@ -433,16 +433,19 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, un
 template <bool BUF>
 __global__ __launch_bounds__(256) void vquant_kernel(const unsigned short* __restrict__ v,
                                                      uint8_t* __restrict__ vhat, VqArgs a) {
-  const int D2 = a.D >> 1;
-  long tid = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  long total = (long)a.B * a.H * a.nb * D2;
+  // thread index: 32-bit with buffer loads (V below 2 GiB, so fewer than
+  // 2^31 threads), which keeps the divisions short
+  typedef typename std::conditional<BUF, unsigned, unsigned long>::type IDX;
+  const int D2 = a.D >> 1;   // 32 or 64
+  const IDX tid = (IDX)blockIdx.x * blockDim.x + threadIdx.x;
+  const IDX total = (IDX)a.B * a.H * a.nb * D2;
   if (tid >= total) return;
-  int dp = (int)(tid % D2);
-  long r = tid / D2;
-  int blk = (int)(r % a.nb);
-  r /= a.nb;
-  int g = (int)(r % a.H);
-  int b = (int)(r / a.H);
+  const int dp = (int)(tid % D2);
+  IDX r = tid / D2;
+  const int blk = (int)(r % (IDX)a.nb);
+  r /= (IDX)a.nb;
+  const int g = (int)(r % (IDX)a.H);
+  const int b = (int)(r / (IDX)a.H);
   const int d0 = 2 * dp;
   // the lane's column pair in the block's 32 rows; rows past S read as 0
   const int nvalid = min(32, a.S - blk * 32);
@@ -504,30 +507,23 @@ struct Q8Args {
   size_t soff;
 };
 
-// E4M3 code of |x| 2^-k for bf16 bits x, with |x| 2^-k < 512: the binade
-// exponent E of y (at least -6, the subnormal binade), the 3-bit mantissa
-// step 2^(E-3), y / step rounded to nearest even (a carry into the next
-// binade yields the right code), saturated to 448.
-__device__ __forceinline__ unsigned e4m3_code(unsigned bits, int k) {
-  const float y = ldexpf(__uint_as_float((bits & 0x7fffu) << 16), -k);
-  const int E = max((int)((__float_as_uint(y) >> 23) & 255u) - 127, -6);
-  const int q = (int)rintf(ldexpf(y, 3 - E));
-  const unsigned c = (unsigned)min(((E + 7) << 3) + q - 8, 0x7E);
-  return c | ((bits >> 8) & 0x80u);
-}
-
-// One thread per 8 elements (4 threads per 32-element block, lanes 4i..4i+3).
+// One thread per 8 elements (4 threads per 32-element block, lanes 4i..4i+3);
+// the rounding is the hardware E4M3 conversion (two elements per
+// instruction) of |x| 2^-k clamped to 448, with the input's sign.
+// IDX: the integer type of the thread and row indices (32-bit whenever the
+// thread count fits, which keeps the divisions short).
+template <typename IDX>
 __global__ __launch_bounds__(256) void mxfp8_kernel(const unsigned short* __restrict__ x,
                                                     uint8_t* __restrict__ y, Q8Args a) {
-  const int parts = a.D / 8;
-  const long n = (long)blockIdx.x * 256 + threadIdx.x;
-  const long row = n / parts;
+  const int parts = a.D / 8;   // 8 or 16
+  const IDX n = (IDX)blockIdx.x * 256 + threadIdx.x;
+  const IDX row = n / parts;
   const int part = (int)(n % parts);
-  if (row >= (long)a.B * a.H * a.s_pad) return;   // whole rows, so whole 4-lane groups
-  const int s = (int)(row % a.s_pad);
-  const long bh = row / a.s_pad;
-  const int h = (int)(bh % a.H);
-  const long b = bh / a.H;
+  if (row >= (IDX)a.B * a.H * a.s_pad) return;   // whole rows, so whole 4-lane groups
+  const int s = (int)(row % (IDX)a.s_pad);
+  const IDX bh = row / (IDX)a.s_pad;
+  const int h = (int)(bh % (IDX)a.H);
+  const long b = (long)(bh / (IDX)a.H);
   u32x4 v = u32x4{0u, 0u, 0u, 0u};
   if (s < a.S) v = *(const u32x4*)(x + ((b * a.S + s) * a.H + h) * a.D + part * 8);
   unsigned am = 0;
@@ -537,9 +533,20 @@ __global__ __launch_bounds__(256) void mxfp8_kernel(const unsigned short* __rest
   am = max(am, (unsigned)__shfl_xor((int)am, 2));
   const int e = (int)(am >> 7);
   const int k = e == 0 ? -127 : max(e - 135, -127);
-  unsigned w[2] = {0u, 0u};
-#pragma unroll
-  for (int j = 0; j < 8; ++j) w[j >> 2] |= e4m3_code((v[j >> 1] >> (16 * (j & 1))) & 0xffffu, k) << (8 * (j & 3));
+  // each pair of elements: y = x 2^-k (exact), clamped to +-448 (the
+  // saturation), then the hardware E4M3 conversion at scale 1 (nearest,
+  // ties to even, sign from the input) into one 16-bit half of a word
+  typedef __attribute__((ext_vector_type(2))) short s16x2;
+  auto y2 = [&](int j, int half) {
+    const unsigned b = half ? (v[j] & 0xffff0000u) : (v[j] << 16);
+    return __builtin_amdgcn_fmed3f(ldexpf(__uint_as_float(b), -k), -448.0f, 448.0f);
+  };
+  s16x2 w0 = {0, 0}, w1 = {0, 0};
+  w0 = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(w0, y2(0, 0), y2(0, 1), 1.0f, false);
+  w0 = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(w0, y2(1, 0), y2(1, 1), 1.0f, true);
+  w1 = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(w1, y2(2, 0), y2(2, 1), 1.0f, false);
+  w1 = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(w1, y2(3, 0), y2(3, 1), 1.0f, true);
+  const unsigned w[2] = {__builtin_bit_cast(unsigned, w0), __builtin_bit_cast(unsigned, w1)};
   *(uint2*)(y + row * a.D + part * 8) = make_uint2(w[0], w[1]);
   if ((part & 3) == 0) y[a.soff + row * (a.D / 32) + (part >> 2)] = (uint8_t)(k + 127);
 }
@@ -1952,8 +1959,13 @@ int launch_q8(const void* x, int B, int S, int H, int D, void* y, hipStream_t st
   const long rows = (long)B * H * a.s_pad;
   a.soff = q8_scale_offset(rows, D);
   const long threads = rows * (D / 8);
-  hipLaunchKernelGGL(mxfp8_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st,
-                     (const unsigned short*)x, (uint8_t*)y, a);
+  const unsigned grid = (unsigned)((threads + 255) / 256);
+  if (threads + 256 < ((long)1 << 32))
+    hipLaunchKernelGGL(mxfp8_kernel<unsigned>, dim3(grid), dim3(256), 0, st,
+                       (const unsigned short*)x, (uint8_t*)y, a);
+  else
+    hipLaunchKernelGGL(mxfp8_kernel<unsigned long>, dim3(grid), dim3(256), 0, st,
+                       (const unsigned short*)x, (uint8_t*)y, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(EFQ_EHIP, "mxfp8 launch: %s", hipGetErrorString(e));
   return EFQ_OK;
