@@ -66,6 +66,35 @@ def test_quant_qk_bitexact(B, orc, S, Hq, Hkv, D):
         assert int(pad.abs().sum()) == 0
 
 
+def test_quant_qk_ties(B, orc):
+    """Exact E4M3 midpoints of x 2^-k in the normal and subnormal binades
+    (ties to the even mantissa), values between 448 and 512 (saturation to
+    448), both signs, block scales 2^-20 .. 2^20: codes and scales equal the
+    oracle's."""
+    vals0 = [1.0625, 1.1875, 9.5, 17.0, 19.0, 304.0, 2.0 ** -10, 3 * 2.0 ** -10, 5 * 2.0 ** -10,
+             7 * 2.0 ** -10, 1.0, 1.125, 288.0, 320.0, 0.0, 2.0 ** -6, 2.0 ** -7, 0.5, 0.5625, 33.0,
+             35.0, 40.0, 44.0, 100.0, 104.0, 136.0, 152.0, 200.0, 208.0, 224.0, 240.0, 448.0]
+    vals1 = [464.0, 480.0, 496.0, 448.0, 416.0, 432.0, 440.0, 400.0, 384.0, 352.0, 336.0] * 3
+    vals1 = vals1[:31] + [496.0]                     # maximum 496: k = e, saturation
+    S, H, D = 64, 1, 64
+    q = torch.zeros(1, S, H, D)
+    for s_ in range(S):
+        e = s_ % 41 - 20
+        sgn = torch.tensor([1.0 if ((j * 5 + s_) % 3) else -1.0 for j in range(32)])
+        q[0, s_, 0, :32] = torch.tensor(vals0) * sgn * 2.0 ** e    # maximum 448: k = e
+        q[0, s_, 0, 32:] = torch.tensor(vals1) * sgn.flip(0) * 2.0 ** e
+    qb = q.to(torch.bfloat16)
+    assert torch.equal(qb.float(), q)              # every value is exact in bf16
+    kb = qb[:, :, :1].clone()
+    sh = B.Shape(1, S, S, H, 1, D)
+    qh, kh = B.quant_qk(qb.cuda(), kb.cuda())
+    qc, qe, kc, ke = _natural(B, qh, kh, sh)
+    for got_c, got_e, x in [(qc, qe, qb), (kc, ke, kb)]:
+        oc, oe = orc.quant_mxfp8(_bhsd(orc.bf16_bits(x)))
+        assert np.array_equal(got_e.cpu().numpy(), oe)
+        assert np.array_equal(got_c.cpu().numpy(), oc)
+
+
 CASES = [
     # (batch, seq_q, seq_k, heads_q, heads_kv, head_dim, causal)
     (1, 256, 256, 2, 1, 64, False),

@@ -101,6 +101,42 @@ def test_vquant_bitexact(B, orc, S, H, D):
     assert int(eg[:, :, nblk:].sum()) == 0
 
 
+def _bf16_next(x: float, up: bool) -> float:
+    """The bf16 neighbour of a bf16-representable positive x."""
+    b = torch.tensor([x], dtype=torch.bfloat16).view(torch.int16)
+    return float((b + (1 if up else -1)).view(torch.bfloat16).float())
+
+
+def test_vquant_ties(B, orc):
+    """Exact E2M1 midpoints of v 2^-k, their bf16 neighbours on both sides,
+    the grid points and the saturation region, with both signs and block
+    scales 2^-20 .. 2^20: the codes (ties to the even code) and scales equal
+    the oracle's."""
+    mids = [0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0]
+    vals0 = []
+    for m in mids:
+        vals0 += [m, _bf16_next(m, True), _bf16_next(m, False)]
+    vals0 += [0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 0.0, 0.125, 0.0625, 0.375]
+    vals0 = vals0[:31] + [6.0]                       # block maximum 6: k = e
+    vals1 = [5.0, 5.5, 5.75, 6.0, 6.5, 7.0, 4.0, 4.5, 3.0, 2.5, 0.25] * 3
+    vals1 = vals1[:31] + [7.5]                       # maximum 7.5: k = e, codes saturate
+    S, H, D = 64, 2, 64
+    v = torch.zeros(1, S, H, D)
+    for h in range(H):
+        for d in range(D):
+            e = (d + 29 * h) % 41 - 20
+            sgn = torch.tensor([1.0 if ((t * 7 + d + h) % 3) else -1.0 for t in range(32)])
+            v[0, :32, h, d] = torch.tensor(vals0) * sgn * 2.0 ** e
+            v[0, 32:, h, d] = torch.tensor(vals1) * sgn.flip(0) * 2.0 ** e
+    vb = v.to(torch.bfloat16)
+    assert torch.equal(vb.float(), v)              # every value is exact in bf16
+    vh = B.quant_v(vb.cuda())
+    cg, eg = B.vhat_natural(vh, B.Shape(1, 1, S, H, H, D))
+    co, eo = orc.quant_v(orc.bf16_bits(vb))
+    assert np.array_equal(eg[:, :, :2].cpu().numpy(), eo)
+    assert np.array_equal(cg[:, :, :64].cpu().numpy(), co)
+
+
 CASES = [
     # (batch, seq_q, seq_k, heads_q, heads_kv, head_dim, causal)
     (1, 256, 256, 2, 1, 64, False),
