@@ -42,6 +42,7 @@ PEAK_BF16 = 2500.0     # TFLOP/s, MI355X dense bf16 MFMA
 PEAK_FP4 = 10100.0     # TFLOP/s, MI355X dense MXFP4 MFMA
 PEAK_FP8 = 5000.0      # TFLOP/s, MI355X dense FP8 MFMA
 PEAK_CLOCK_GHZ = 2.4   # the clock the peaks are quoted at
+PEAK_HBM = 8.0         # TB/s, MI355X HBM3E
 N_CU = 256
 COPY_BYTES = 1 << 30   # plain copy used to scale the HBM counters
 
@@ -282,6 +283,13 @@ def main():
             kclk = round(phases.kernel_sclk(w, q, k, vhat, out), 3) or None
             binding.lib()
     sclk = measure_sclk(binding, stream)
+    # the V quantiser alone, 20 launches back to back (its HBM roofline)
+    def vq():
+        binding.quant_v(v, seq_q=w.seq, heads_q=w.heads_q, out=vhat, stream=stream)
+    vq()
+    torch.cuda.synchronize()
+    vq_loop_ms = _time_calls(vq, 20, stream)
+    vq_bytes = v.numel() * 2 + vhat.numel()
     flops = w.flops()
     value = flops / (ms_step * 1e-3) / 1e12
     achieved = flops / (attn_ms * 1e-3) / 1e12
@@ -336,6 +344,11 @@ def main():
                                             if sclk > 0 else None),
         },
         "vquant_ms": round(vq_ms, 4),
+        "vquant": {"bound": "hbm", "us_per_launch": round(vq_loop_ms * 1e3, 2),
+                   "bytes": vq_bytes,
+                   "achieved_tbps": round(vq_bytes / (vq_loop_ms * 1e-3) / 1e12, 3),
+                   "peak_tbps": PEAK_HBM,
+                   "frac": round(vq_bytes / (vq_loop_ms * 1e-3) / 1e12 / PEAK_HBM, 4)},
     }
 
     if not args.no_extra:
@@ -521,7 +534,11 @@ def lowbit_run(w, binding, q, k, v, vhat, out, stream, steps):
 
     def prepass():
         binding.quant_qk(q, k, stream=stream)
-    res["qk_prepass_ms"] = round(_time_calls(prepass, n, stream), 4)
+    pms = _time_calls(prepass, n, stream)
+    pbytes = (q.numel() + k.numel()) * 2 + qh.numel() + kh.numel()
+    res["qk_prepass_ms"] = round(pms, 4)
+    res["qk_prepass_tbps"] = round(pbytes / (pms * 1e-3) / 1e12, 3)
+    res["qk_prepass_frac_hbm"] = round(pbytes / (pms * 1e-3) / 1e12 / PEAK_HBM, 4)
     ws = torch.empty(binding.lowbit_workspace_bytes(sh) + 256, dtype=torch.uint8, device=q.device)
     off = (-ws.data_ptr()) % 256
     wsv = ws[off: off + binding.lowbit_workspace_bytes(sh)]
