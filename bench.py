@@ -534,6 +534,8 @@ def lowbit_run(w, binding, q, k, v, vhat, out, stream, steps):
 
     def prepass():
         binding.quant_qk(q, k, stream=stream)
+    prepass()   # its output buffers come from the allocator's cache from here on
+    torch.cuda.synchronize()
     pms = _time_calls(prepass, n, stream)
     pbytes = (q.numel() + k.numel()) * 2 + qh.numel() + kh.numel()
     res["qk_prepass_ms"] = round(pms, 4)
