@@ -116,7 +116,7 @@ def test_fullsize_all_rows_in_value_hull(B, wl):
         lo, hi = vq.amin(dim=2, keepdim=True), vq.amax(dim=2, keepdim=True)
     del vq
     group = w.heads_q // w.heads_kv
-    for kind in ("efq", "expq"):
+    for kind in ("efq", "lut", "expq", "expq6"):
         out = B.attn_fwd_vhat(q, k, vh, w.scale, w.causal, kind)
         torch.cuda.synchronize()
         worst = 0.0
