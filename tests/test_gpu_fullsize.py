@@ -93,7 +93,8 @@ def test_fullsize_sampled_rows(B, orc, wl):
 @pytest.mark.parametrize("wl", ["qwen3_8b_16k", "qwen3_8b_32k", "qwen3_8b_128k", "qwen3_vl_32k",
                                 "wan22_75600"])
 def test_fullsize_all_rows_in_value_hull(B, wl):
-    """Every row at full size, by a property that holds at any size: P~ >= 0
+    """Every row at full size, every probability stage, both Q K^T paths, by
+    a property that holds at any size: P~ >= 0
     and O = (P~ V~) / (P~ 1), so each output element lies between the
     smallest and the largest dequantised V~ value of that column over the
     row's visible keys (a prefix for causal rows).  Catches a wrong kv head,
@@ -116,8 +117,15 @@ def test_fullsize_all_rows_in_value_hull(B, wl):
         lo, hi = vq.amin(dim=2, keepdim=True), vq.amax(dim=2, keepdim=True)
     del vq
     group = w.heads_q // w.heads_kv
-    for kind in ("efq", "lut", "expq", "expq6"):
-        out = B.attn_fwd_vhat(q, k, vh, w.scale, w.causal, kind)
+    sh = B.shape_of(q, k)
+    qh, kh = B.quant_qk(q, k)
+    runs = [(kind, lambda kind=kind: B.attn_fwd_vhat(q, k, vh, w.scale, w.causal, kind))
+            for kind in ("efq", "lut", "expq", "expq6")]
+    runs += [("lowbit " + kind,
+              lambda kind=kind: B.attn_fwd_qk8(qh, kh, vh, sh, w.scale, w.causal, kind))
+             for kind in ("efq", "expq")]
+    for kind, run in runs:
+        out = run()
         torch.cuda.synchronize()
         worst = 0.0
         for hq in range(w.heads_q):
