@@ -1186,12 +1186,10 @@ struct PPWave {
                                 : KIND == EFQ_PGEN_NOOP ? 0 : EFQ_PRIO_OTHER_V;
   // The P~V and P~1 MFMAs have no memory effects, so the compiler may sink
   // them past the phase barrier into the VALU phase, next to their first
-  // use.  On the FP8 Q K^T path the stages whose matrix phase is the
-  // heavier one (exp-then-quantize, the no-op stage) issue them in the
-  // matrix phase instead (an empty asm reads their results there); EFQ and
-  // LUT, and every stage on the bf16 path, keep the compiler's placement.
-  // Measured, both ways.
-  static constexpr bool kPvFence = Q8 && KIND != EFQ_PGEN_EFQ && KIND != EFQ_PGEN_LUT;
+  // use.  On the FP8 Q K^T path every stage issues them in the matrix phase
+  // instead (an empty asm reads their results there); every stage on the
+  // bf16 path keeps the compiler's placement.  Measured, both ways.
+  static constexpr bool kPvFence = Q8;
 
   // Matrix phase M(j): with QK the scores of tile j into sn, and with CODES
   // the codes of tile j-1 (scores sc) in the shadow of those MFMAs, then its
