@@ -1308,10 +1308,11 @@ __device__ __forceinline__ void pp_schedule(PPWave<D, KIND, DUMP, Q8>& w, int T,
   int vr = 0;          // V~ slot of the next VALU phase
   auto knext = [](int x) { return ring_next<Sm::kK, kPPK>(x); };
   auto vnext = [](int x) { return ring_next<Sm::kV, kPPV>(x); };
-  // bf16 Q K^T: the tile loads go out after the even phase's work, not
-  // before it (measured 1.5 % faster; the MXFP8 path is faster with them
-  // first).  Either way they belong to phase t, as the schedule assumes.
-  constexpr bool kLate = !Q8;
+  // The tile loads go out after the even phase's work, not before it, on
+  // the bf16 path (measured 1.5 % faster) and for EFQ on the MXFP8 path
+  // (2.8 %); the other MXFP8 stages are as fast or faster with them first.
+  // Either way they belong to phase t, as the schedule assumes.
+  constexpr bool kLate = !Q8 || KIND == EFQ_PGEN_EFQ;
   // Phase t with TM = t % 4 known (even TM only for t >= 2); TM = 4 is t = 0.
   auto begin = [&](auto tm) {
     constexpr int TM = decltype(tm)::value;
